@@ -1,0 +1,169 @@
+"""The fp64 CPU oracle of the selective scan -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product path (the HIP library and
+its Python binding) never calls it, and it never calls the product path.
+
+The arithmetic lives in ``mbscan_oracle.c`` (plain C, IEEE double, built by
+gcc without fast-math).  This wrapper only decodes the input formats (bf16 bit
+patterns and fp32 widen exactly to fp64), arranges rows and hands pointers to
+the C code.  See the C file for what is computed and which passage of the paper
+each step follows.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "mbscan_oracle.c")
+LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+_D = ctypes.POINTER(ctypes.c_double)
+_I64 = ctypes.POINTER(ctypes.c_int64)
+
+
+def build(src: str = _SRC, out: str = LIB_PATH, extra_flags=()) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP, no fast-math)."""
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
+           *extra_flags, "-o", out, src, "-lm"]
+    subprocess.run(cmd, check=True)
+    return out
+
+
+def to_f64(x, dtype: str | None = None) -> np.ndarray:
+    """Exact widening to fp64.  ``dtype="bf16"`` means x holds bf16 bit patterns."""
+    x = np.asarray(x)
+    if dtype == "bf16" or x.dtype == np.uint16:
+        bits = np.ascontiguousarray(x, dtype=np.uint16).astype(np.uint32) << 16
+        return bits.view(np.float32).astype(np.float64)
+    return np.ascontiguousarray(x, dtype=np.float64)
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(_D)
+
+
+class Oracle:
+    """ctypes handle on a built oracle library (the default one, or a test build)."""
+
+    def __init__(self, lib_path: str = LIB_PATH):
+        if not os.path.exists(lib_path):
+            build(out=lib_path)
+        self.lib = ctypes.CDLL(lib_path)
+        self.lib.mbo_scan_rows.restype = ctypes.c_int
+        self.lib.mbo_scan_rows.argtypes = [
+            ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+            _D, _D, _D, _D, _D, _D, _D, _I64, ctypes.c_int64, _D, _D, _D, _D]
+        self.lib.mbo_scan_step.restype = ctypes.c_int
+        self.lib.mbo_scan_step.argtypes = [
+            ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+            _D, _D, _D, _D, _D, _D, _I64, ctypes.c_int64, _D, _D, _D, _D]
+
+    # -- rows ---------------------------------------------------------------
+    def scan_rows(self, u, delta, A, Bm, Cm, bidx, *, z=None, Dskip=None, dt_bias=None,
+                  h0=None, delta_softplus=True, want_h_last=True):
+        """Scan R independent rows.
+
+        u, delta, z: (R, L); A, h0: (R, N); Dskip, dt_bias: (R,);
+        Bm, Cm: (nbatch, N, L); bidx: (R,) batch index of each row.
+        All float arguments must already be fp64.  Returns (y (R, L), h_last (R, N) or None).
+        """
+        u = np.ascontiguousarray(u, dtype=np.float64)
+        R, L = u.shape
+        Bm = np.ascontiguousarray(Bm, dtype=np.float64)
+        nb, N, Lb = Bm.shape
+        if Lb != L:
+            raise ValueError("B/C length does not match u")
+        args = dict(delta=delta, z=z, A=A, Dskip=Dskip, dt_bias=dt_bias, h0=h0, Cm=Cm)
+        a = {k: (None if v is None else np.ascontiguousarray(v, dtype=np.float64))
+             for k, v in args.items()}
+        bidx = np.ascontiguousarray(bidx, dtype=np.int64)
+        y = np.empty((R, L), dtype=np.float64)
+        h_last = np.empty((R, N), dtype=np.float64) if want_h_last else None
+        rc = self.lib.mbo_scan_rows(R, L, N, int(bool(delta_softplus)),
+                                    _ptr(u), _ptr(a["delta"]), _ptr(a["z"]), _ptr(a["A"]),
+                                    _ptr(a["Dskip"]), _ptr(a["dt_bias"]), _ptr(a["h0"]),
+                                    bidx.ctypes.data_as(_I64), nb, _ptr(Bm), _ptr(a["Cm"]),
+                                    _ptr(y), _ptr(h_last))
+        if rc != 0:
+            raise ValueError(f"oracle rejected the arguments (status {rc})")
+        return y, h_last
+
+    # -- whole tensors --------------------------------------------------------
+    def scan_fwd(self, u, delta, A, Bm, Cm, *, z=None, Dskip=None, dt_bias=None, h0=None,
+                 delta_softplus=True, dtype: str | None = None, rows=None):
+        """Scan (batch, dim, L) tensors; ``rows`` optionally picks flat (b*dim + d) rows.
+
+        Activations may be bf16 bit patterns (``dtype="bf16"``) or floats.
+        Returns y of shape (batch, dim, L) -- or (len(rows), L) -- and h_last
+        of shape (batch, dim, N) -- or (len(rows), N) -- in fp64.
+        """
+        u = np.asarray(u)
+        nb, dim, L = u.shape
+        N = np.asarray(A).shape[1]
+        flat = np.arange(nb * dim) if rows is None else np.asarray(rows, dtype=np.int64)
+        bidx = flat // dim
+        didx = flat % dim
+
+        def act(x):
+            return None if x is None else to_f64(np.asarray(x).reshape(nb * dim, -1)[flat], dtype)
+
+        Af = to_f64(A)[didx]
+        y, h_last = self.scan_rows(
+            act(u), act(delta), Af, to_f64(Bm, dtype), to_f64(Cm, dtype), bidx,
+            z=act(z),
+            Dskip=None if Dskip is None else to_f64(Dskip)[didx],
+            dt_bias=None if dt_bias is None else to_f64(dt_bias)[didx],
+            h0=None if h0 is None else to_f64(h0).reshape(nb * dim, N)[flat],
+            delta_softplus=delta_softplus)
+        if rows is None:
+            return y.reshape(nb, dim, L), h_last.reshape(nb, dim, N)
+        return y, h_last
+
+    def scan_step(self, h, u_t, delta_t, A, B_t, C_t, *, z_t=None, Dskip=None, dt_bias=None,
+                  delta_softplus=True, dtype: str | None = None):
+        """One step for (batch, dim) inputs; returns (y_t (batch, dim), new h (batch, dim, N))."""
+        h_new = np.array(to_f64(h), dtype=np.float64, copy=True)
+        nb, dim, N = h_new.shape
+        R = nb * dim
+        bidx = np.repeat(np.arange(nb, dtype=np.int64), dim)
+        didx = np.tile(np.arange(dim), nb)
+
+        def flat(x):
+            return None if x is None else to_f64(x, dtype).reshape(R)
+
+        y = np.empty(R, dtype=np.float64)
+        Af = np.ascontiguousarray(to_f64(A)[didx])
+        Ds = None if Dskip is None else np.ascontiguousarray(to_f64(Dskip)[didx])
+        db = None if dt_bias is None else np.ascontiguousarray(to_f64(dt_bias)[didx])
+        hv = h_new.reshape(R, N)
+        ut, dtt, zt = flat(u_t), flat(delta_t), flat(z_t)
+        Bt = np.ascontiguousarray(to_f64(B_t, dtype).reshape(nb, N))
+        Ct = np.ascontiguousarray(to_f64(C_t, dtype).reshape(nb, N))
+        rc = self.lib.mbo_scan_step(R, N, int(bool(delta_softplus)), _ptr(ut), _ptr(dtt), _ptr(zt),
+                                    _ptr(Af), _ptr(Ds), _ptr(db), bidx.ctypes.data_as(_I64), nb,
+                                    _ptr(Bt), _ptr(Ct), _ptr(hv), _ptr(y))
+        if rc != 0:
+            raise ValueError(f"oracle rejected the arguments (status {rc})")
+        return y.reshape(nb, dim), h_new
+
+
+_default = None
+
+
+def default() -> Oracle:
+    global _default
+    if _default is None:
+        _default = Oracle()
+    return _default
+
+
+def scan_inputs(inp, rows=None, delta_softplus=True):
+    """Run the oracle on a ``ScanInputs`` workload (any object with the same fields)."""
+    return default().scan_fwd(inp.u, inp.delta, inp.A, inp.B, inp.C, z=inp.z, Dskip=inp.Dskip,
+                              dt_bias=inp.dt_bias, h0=inp.h0, delta_softplus=delta_softplus,
+                              dtype=inp.dtype, rows=rows)

@@ -1,0 +1,14 @@
+"""MI355X-native selective scan (the S6 scan at the heart of every MambaByte layer).
+
+The compute path is the HIP library ``libmbscan.so`` (hand-written gfx950
+kernels behind a C ABI declared in ``include/mbscan.h``); this package is a thin
+binding over it.  ``scan_fwd`` and ``scan_step`` are loaded on first use.
+"""
+__all__ = ["scan_fwd", "scan_step", "load_library", "MBScanError"]
+
+
+def __getattr__(name):
+    if name in __all__:
+        from . import _binding
+        return getattr(_binding, name)
+    raise AttributeError(name)

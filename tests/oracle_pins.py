@@ -1,0 +1,310 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+Each ``pin_*`` function takes an ``oracle.Oracle`` and raises AssertionError
+when the oracle disagrees.  None of them re-types the oracle's recurrence:
+they use the continuous-time closed form on the grid t_k = sum Delta
+(Section 2 after eq. (2)), the geometric series, special cases with textbook
+answers (Appendix D, eq. (4); the Delta limits stated after it), the
+associative tuple scan of Section 2 "Implementation", and structural
+invariants (split/resume, state separability, linearity, step == forward).
+``tests/test_oracle_mutants.py`` checks that these pins catch plausible bugs.
+"""
+from __future__ import annotations
+
+import json
+import os
+from decimal import Decimal
+
+import numpy as np
+from scipy.special import expit
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "bruteforce_tiny.json")
+
+
+def _softplus_ref(v):
+    # log(1 + e^v) as log(e^0 + e^v): a library routine, not the oracle's log1p form.
+    return np.logaddexp(0.0, v)
+
+
+def _relerr(g, r):
+    g = np.asarray(g, np.float64).ravel()
+    r = np.asarray(r, np.float64).ravel()
+    den = np.abs(r) + np.sqrt(np.mean(r * r)) + 1e-300
+    return float(np.max(np.abs(g - r) / den))
+
+
+def _close(g, r, tol, what):
+    e = _relerr(g, r)
+    assert e <= tol, f"{what}: relative error {e:.3e} > {tol:.1e}"
+
+
+def _rand_case(seed, nb=2, dim=3, L=40, N=4, *, gated=True, h0=True, D=True, bias=True):
+    rng = np.random.default_rng(seed)
+    c = dict(
+        u=rng.standard_normal((nb, dim, L)),
+        delta=rng.standard_normal((nb, dim, L)),
+        A=-rng.uniform(0.1, 4.0, (dim, N)),
+        B=rng.standard_normal((nb, N, L)),
+        C=rng.standard_normal((nb, N, L)),
+        z=rng.standard_normal((nb, dim, L)) if gated else None,
+        Dskip=rng.uniform(0.5, 1.5, dim) if D else None,
+        dt_bias=rng.uniform(-3.0, 0.5, dim) if bias else None,
+        h0=0.5 * rng.standard_normal((nb, dim, N)) if h0 else None,
+    )
+    return c
+
+
+def _run(orc, c, **kw):
+    return orc.scan_fwd(c["u"], c["delta"], c["A"], c["B"], c["C"], z=c["z"], Dskip=c["Dskip"],
+                        dt_bias=c["dt_bias"], h0=c["h0"], **kw)
+
+
+def _brute(c, delta_softplus=True):
+    """Time-grid closed form of every state (eq. (1) solved on t_k = sum Delta)."""
+    u, A, Bm, Cm = c["u"], c["A"], c["B"], c["C"]
+    nb, dim, L = u.shape
+    N = A.shape[1]
+    y = np.zeros((nb, dim, L))
+    h_last = np.zeros((nb, dim, N))
+    for b in range(nb):
+        for d in range(dim):
+            v = c["delta"][b, d] + (0.0 if c["dt_bias"] is None else c["dt_bias"][d])
+            dl = _softplus_ref(v) if delta_softplus else v
+            S = np.cumsum(dl)                       # S_t = t-th grid point
+            h0 = np.zeros(N) if c["h0"] is None else c["h0"][b, d]
+            for t in range(L):
+                w = np.exp(np.outer(A[d], S[t] - S[: t + 1]))          # (N, t+1) decay from s to t
+                inp = dl[: t + 1] * Bm[b, :, : t + 1] * u[b, d, : t + 1]  # Euler B-bar x at each s
+                h = np.exp(A[d] * S[t]) * h0 + (w * inp).sum(axis=1)
+                yv = Cm[b, :, t] @ h + (0.0 if c["Dskip"] is None else c["Dskip"][d]) * u[b, d, t]
+                if c["z"] is not None:
+                    zz = c["z"][b, d, t]
+                    yv = yv * zz * expit(zz)
+                y[b, d, t] = yv
+            h_last[b, d] = h if L > 0 else h0
+    return y, h_last
+
+
+# ---------------------------------------------------------------------------
+
+def pin_golden_decimal(orc):
+    """50-digit time-grid fixtures (tests/golden/bruteforce_tiny.json)."""
+    with open(GOLDEN) as f:
+        cases = json.load(f)
+    for cs in cases:
+        L, N = cs["L"], cs["N"]
+        arr = lambda k, shape: np.array([float(v) for v in cs[k]]).reshape(shape)
+        y, h = orc.scan_fwd(arr("u", (1, 1, L)), arr("delta", (1, 1, L)), arr("A", (1, N)),
+                            arr("B", (1, N, L)), arr("C", (1, N, L)),
+                            z=None if cs["z"] is None else arr("z", (1, 1, L)),
+                            Dskip=np.array([float(cs["Dskip"])]),
+                            dt_bias=np.array([float(cs["dt_bias"])]),
+                            h0=None if cs["h0"] is None else arr("h0", (1, 1, N)),
+                            delta_softplus=cs["delta_softplus"])
+        ry = np.array([float(Decimal(v)) for v in cs["y"]])
+        rh = np.array([float(Decimal(v)) for v in cs["h_last"]])
+        _close(y.ravel(), ry, 1e-13, f"golden {cs['name']} y")
+        _close(h.ravel(), rh, 1e-13, f"golden {cs['name']} h_last")
+
+
+def pin_bruteforce(orc):
+    """Oracle == time-grid materialisation on small random inputs (several batches)."""
+    for seed, kw in ((1, {}), (2, dict(gated=False, h0=False)), (3, dict(D=False, bias=False))):
+        c = _rand_case(seed, **kw)
+        y, h = _run(orc, c)
+        ry, rh = _brute(c)
+        _close(y, ry, 1e-11, f"bruteforce y seed {seed}")
+        _close(h, rh, 1e-11, f"bruteforce h_last seed {seed}")
+    # softplus off: Delta = delta_raw + bias, used as given (kept positive here)
+    c = _rand_case(4)
+    rng = np.random.default_rng(40)
+    c["delta"] = rng.uniform(0.01, 0.3, c["u"].shape)
+    c["dt_bias"] = rng.uniform(0.0, 0.05, c["A"].shape[0])
+    y, h = _run(orc, c, delta_softplus=False)
+    ry, rh = _brute(c, delta_softplus=False)
+    _close(y, ry, 1e-11, "bruteforce (no softplus) y")
+    _close(h, rh, 1e-11, "bruteforce (no softplus) h_last")
+
+
+def pin_geometric(orc):
+    """Constant Delta, B, x, C: h_t = a^(t+1) h0 + b (1 - a^(t+1)) / (1 - a)."""
+    L, N = 300, 5
+    A = -np.array([[0.05, 0.3, 1.0, 2.5, 7.0]])
+    v, bias, x, Bv, Cv, D = 0.4, -1.1, 0.7, np.array([0.9, -1.3, 0.25, 2.0, -0.6]), \
+        np.array([1.5, 0.2, -0.8, 0.33, 1.1]), 0.6
+    h0 = np.array([0.3, -0.2, 1.0, 0.0, -0.7])
+    dlt = float(np.logaddexp(0.0, v + bias))
+    a = np.exp(dlt * A[0])
+    b = dlt * Bv * x
+    t = np.arange(L)[:, None]
+    h_ref = a ** (t + 1) * h0 + b * (1 - a ** (t + 1)) / (1 - a)        # (L, N)
+    y_ref = h_ref @ Cv + D * x
+    y, h = orc.scan_fwd(np.full((1, 1, L), x), np.full((1, 1, L), v), A,
+                        np.repeat(Bv[None, :, None], L, axis=2), np.repeat(Cv[None, :, None], L, axis=2),
+                        Dskip=np.array([D]), dt_bias=np.array([bias]), h0=h0[None, None])
+    _close(y.ravel(), y_ref, 1e-12, "geometric y")
+    _close(h.ravel(), h_ref[-1], 1e-12, "geometric h_last")
+
+
+def pin_B_zero(orc):
+    """B = 0: with h0 = 0 the output is D x silu(z); with h0 the state only decays."""
+    c = _rand_case(5, h0=False)
+    c["B"] = np.zeros_like(c["B"])
+    y, h = _run(orc, c)
+    ref = c["Dskip"][None, :, None] * c["u"] * c["z"] * expit(c["z"])
+    _close(y, ref, 1e-15, "B=0 y")
+    assert np.all(h == 0.0), "B=0, h0=0: state must stay exactly zero"
+    c = _rand_case(6, gated=False)
+    c["B"] = np.zeros_like(c["B"])
+    y, h = _run(orc, c)
+    dl = _softplus_ref(c["delta"] + c["dt_bias"][None, :, None])
+    S = np.cumsum(dl, axis=2)                                             # (nb, dim, L)
+    hs = np.exp(c["A"][None, :, :, None] * S[:, :, None, :]) * c["h0"][..., None]  # (nb,dim,N,L)
+    ry = np.einsum("bnl,bdnl->bdl", c["C"], hs) + c["Dskip"][None, :, None] * c["u"]
+    _close(y, ry, 1e-13, "B=0 decaying h0 y")
+    _close(h, hs[..., -1], 1e-13, "B=0 decaying h0 h_last")
+
+
+def pin_split(orc):
+    """Resume: scan[0:L] == scan[0:k] followed by scan[k:L] started from its h_last."""
+    c = _rand_case(7, L=50)
+    y, h = _run(orc, c)
+    for k in (0, 1, 17, 49, 50):
+        c1 = dict(c, u=c["u"][..., :k], delta=c["delta"][..., :k], z=c["z"][..., :k],
+                  B=c["B"][..., :k], C=c["C"][..., :k])
+        y1, h1 = _run(orc, c1)
+        c2 = dict(c, u=c["u"][..., k:], delta=c["delta"][..., k:], z=c["z"][..., k:],
+                  B=c["B"][..., k:], C=c["C"][..., k:], h0=h1)
+        y2, h2 = _run(orc, c2)
+        _close(np.concatenate([y1, y2], axis=2), y, 1e-13, f"split at {k}: y")
+        _close(h2, h, 1e-13, f"split at {k}: h_last")
+
+
+def pin_eq4(orc):
+    """Appendix D, eq. (4): A = -1, N = 1 gives Abar = 1/(1 + e^v) = sigmoid(-v) = 1 - sigmoid(v).
+
+    Observed through the oracle with B = 0, C = 1, h0 = 1, D = 0, no gate, L = 1
+    (then y = Abar), and over a sequence with B = 1 where the scan must equal
+    the gated recurrence h[k] = (1 - sigmoid(v_k)) h[k-1] + softplus(v_k) x[k]
+    (the simplified-Euler B-bar = Delta replaces the ZOH B-bar of eq. (4))."""
+    v = np.linspace(-30.0, 30.0, 241)
+    R = v.size
+    bias = 0.3
+    y, _ = orc.scan_rows(np.ones((R, 1)), (v - bias)[:, None], -np.ones((R, 1)),
+                         np.zeros((1, 1, 1)), np.ones((1, 1, 1)), np.zeros(R, np.int64),
+                         dt_bias=np.full(R, bias), h0=np.ones((R, 1)))
+    _close(y[:, 0], expit(-v), 1e-14, "eq.(4) Abar = sigmoid(-v)")
+    _close(y[:, 0], 1.0 - expit(v), 1e-9, "eq.(4) Abar = 1 - sigmoid(v)")
+    rng = np.random.default_rng(8)
+    L = 64
+    vs = rng.uniform(-6, 6, L)
+    xs = rng.standard_normal(L)
+    y, h = orc.scan_fwd(xs[None, None], vs[None, None], -np.ones((1, 1)), np.ones((1, 1, L)),
+                        np.ones((1, 1, L)), h0=np.full((1, 1, 1), 0.25))
+    hh, ref = 0.25, []
+    for k in range(L):
+        hh = (1.0 - expit(vs[k])) * hh + _softplus_ref(vs[k]) * xs[k]
+        ref.append(hh)
+    _close(y.ravel(), ref, 1e-12, "eq.(4) gated recurrence")
+
+
+def pin_tuple_scan(orc):
+    """Section 2 "Implementation": a Hillis-Steele scan with e_j . e_k = (A_k A_j, A_k b_j + b_k)."""
+    c = _rand_case(9, nb=1, dim=2, L=37, N=3, gated=False)
+    y, h = _run(orc, c)
+    nb, dim, L = c["u"].shape
+    for d in range(dim):
+        dl = _softplus_ref(c["delta"][0, d] + c["dt_bias"][d])
+        a = np.exp(np.outer(dl, c["A"][d]))                               # (L, N)
+        b = dl[:, None] * c["B"][0].T * c["u"][0, d][:, None]              # (L, N)
+        # prepend the carried state as the element (1, h0)
+        a = np.vstack([np.ones((1, a.shape[1])), a])
+        b = np.vstack([c["h0"][0, d][None], b])
+        off = 1
+        while off < a.shape[0]:
+            a_new, b_new = a.copy(), b.copy()
+            a_new[off:] = a[off:] * a[:-off]
+            b_new[off:] = a[off:] * b[:-off] + b[off:]
+            a, b, off = a_new, b_new, off * 2
+        hs = b[1:]                                                         # (L, N) states
+        ry = (hs * c["C"][0].T).sum(axis=1) + c["Dskip"][d] * c["u"][0, d]
+        _close(y[0, d], ry, 1e-12, "tuple scan y")
+        _close(h[0, d], hs[-1], 1e-12, "tuple scan h_last")
+
+
+def pin_separability(orc):
+    """Only C couples the states: y(N states, D=0) = sum_n y(state n alone)."""
+    c = _rand_case(10, gated=False, D=False)
+    y, h = _run(orc, c)
+    acc = np.zeros_like(y)
+    for n in range(c["A"].shape[1]):
+        cn = dict(c, A=c["A"][:, n:n + 1], B=c["B"][:, n:n + 1], C=c["C"][:, n:n + 1],
+                  h0=c["h0"][..., n:n + 1])
+        yn, hn = _run(orc, cn)
+        acc += yn
+        _close(hn[..., 0], h[..., n], 1e-14, f"separability h_last state {n}")
+    _close(acc, y, 1e-12, "separability y")
+
+
+def pin_linearity(orc):
+    """With h0 = 0 and no gate, y is linear in x for a fixed Delta."""
+    c1 = _rand_case(11, gated=False, h0=False)
+    c2 = dict(c1, u=np.random.default_rng(12).standard_normal(c1["u"].shape))
+    al, be = 0.75, -1.5
+    c3 = dict(c1, u=al * c1["u"] + be * c2["u"])
+    y1, h1 = _run(orc, c1)
+    y2, h2 = _run(orc, c2)
+    y3, h3 = _run(orc, c3)
+    _close(y3, al * y1 + be * y2, 1e-12, "linearity y")
+    _close(h3, al * h1 + be * h2, 1e-12, "linearity h_last")
+
+
+def pin_step_equals_fwd(orc):
+    """L recurrent steps (the generation mode of Section 2) == one forward scan."""
+    c = _rand_case(13, L=20)
+    y, h = _run(orc, c)
+    hh = c["h0"]
+    ys = []
+    for t in range(c["u"].shape[2]):
+        yt, hh = orc.scan_step(hh, c["u"][..., t], c["delta"][..., t], c["A"], c["B"][..., t],
+                               c["C"][..., t], z_t=c["z"][..., t], Dskip=c["Dskip"],
+                               dt_bias=c["dt_bias"])
+        ys.append(yt)
+    _close(np.stack(ys, axis=2), y, 1e-15, "step x L == fwd: y")
+    _close(hh, h, 1e-15, "step x L == fwd: h")
+
+
+def pin_limits(orc):
+    """After eq. (4): Delta -> 0 keeps the state; Delta -> inf forgets it (h -> Delta B x under Euler)."""
+    c = _rand_case(14, gated=False, bias=False, L=16)
+    c["delta"] = np.full_like(c["u"], -45.0)                               # Delta ~ 3e-20
+    y, h = _run(orc, c)
+    _close(h, c["h0"], 1e-15, "Delta->0: h_last == h0")
+    ry = np.einsum("bnl,bdn->bdl", c["C"], c["h0"]) + c["Dskip"][None, :, None] * c["u"]
+    _close(y, ry, 1e-15, "Delta->0: y == C h0 + D x")
+    c["delta"] = np.full_like(c["u"], 45.0)                                # Abar = exp(-45 |A|) ~ 0
+    c["A"] = np.minimum(c["A"], -1.0)
+    y, h = _run(orc, c)
+    ref_h = 45.0 * c["B"][:, None, :, -1] * c["u"][..., -1:]               # (nb, dim, N)
+    _close(h, ref_h, 1e-15, "Delta->inf: h == Delta B x")
+
+
+def pin_softplus_extremes(orc):
+    """softplus(v) over [-80, 80] observed as h after one step with A = 0, B = 1, x = 1."""
+    v = np.concatenate([np.linspace(-80, 80, 321), [-740.0, 0.0, 1e-8, 700.0, 720.0]])
+    R = v.size
+    y, h = orc.scan_rows(np.ones((R, 1)), v[:, None], np.zeros((R, 1)), np.ones((1, 1, 1)),
+                         np.zeros((1, 1, 1)), np.zeros(R, np.int64))
+    ref = _softplus_ref(v)
+    _close(h[:, 0], ref, 1e-15, "softplus")
+    # softplus > 0 everywhere: also hold every value to a plain relative bound, so
+    # that a form which underflows or overflows (log(1 + e^v)) cannot hide.
+    rel = np.max(np.abs(h[:, 0] - ref) / ref)
+    assert rel <= 1e-14, f"softplus elementwise relative error {rel:.3e}"
+
+
+ALL_PINS = [
+    pin_golden_decimal, pin_bruteforce, pin_geometric, pin_B_zero, pin_split, pin_eq4,
+    pin_tuple_scan, pin_separability, pin_linearity, pin_step_equals_fwd, pin_limits,
+    pin_softplus_extremes,
+]

@@ -1,0 +1,78 @@
+"""Plant plausible mistakes in a copy of the oracle (on the CPU) and check that
+at least one pin fails for each: the pins are strong enough to trust the oracle.
+"""
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+
+import pytest
+
+import oracle
+import oracle_pins as P
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "mbscan_oracle.c")
+
+# (name, exact text in the oracle, replacement)
+MUTANTS = [
+    ("drop_skip", "acc + (Dskip ? Dskip[r] * x : 0.0)", "acc"),
+    ("skip_uses_delta", "Dskip[r] * x", "Dskip[r] * dlt"),
+    ("exp_sign", "exp(dlt * A[r * N + n])", "exp(-dlt * A[r * N + n])"),
+    ("exp_without_delta", "exp(dlt * A[r * N + n])", "exp(A[r * N + n])"),
+    ("B_index_prev_t", "Bm[(b * N + n) * L + t]", "Bm[(b * N + n) * L + (t > 0 ? t - 1 : 0)]"),
+    ("B_transposed", "Bm[(b * N + n) * L + t]", "Bm[(b * L + t) * N + n]"),
+    ("C_transposed", "Cm[(b * N + n) * L + t]", "Cm[(b * L + t) * N + n]"),
+    ("B_C_swapped", "const double bbar_x = (dlt * Bm[", "const double bbar_x = (dlt * Cm["),
+    ("y_before_update", "h[n] = abar * h[n] + bbar_x;\n            acc += Cm[(b * N + n) * L + t] * h[n];",
+     "acc += Cm[(b * N + n) * L + t] * h[n];\n            h[n] = abar * h[n] + bbar_x;"),
+    ("zoh_B", "const double bbar_x = (dlt * Bm[(b * N + n) * L + t]) * x;",
+     "const double bbar_x = ((abar - 1.0) / A[r * N + n] * Bm[(b * N + n) * L + t]) * x;"),
+    ("euler_missing_x", "(dlt * Bm[(b * N + n) * L + t]) * x;", "(dlt * Bm[(b * N + n) * L + t]);"),
+    ("euler_missing_delta", "(dlt * Bm[(b * N + n) * L + t]) * x;", "(Bm[(b * N + n) * L + t]) * x;"),
+    ("no_bias", "delta[r * L + t] + (dt_bias ? dt_bias[r] : 0.0)", "delta[r * L + t]"),
+    ("bias_sign", "delta[r * L + t] + (dt_bias ? dt_bias[r] : 0.0)", "delta[r * L + t] - (dt_bias ? dt_bias[r] : 0.0)"),
+    ("softplus_sign", "log1p(exp(-fabs(v)))", "log1p(exp(fabs(v)))"),
+    ("softplus_no_max", "fmax(v, 0.0) + log1p", "log1p"),
+    ("softplus_naive_log", "fmax(v, 0.0) + log1p(exp(-fabs(v)))", "log(1.0 + exp(v))"),
+    ("no_gate", "z ? yv * silu(z[r * L + t]) : yv", "yv"),
+    ("gate_sigmoid_only", "return z / (1.0 + exp(-z));", "return 1.0 / (1.0 + exp(-z));"),
+    ("gate_wrong_sign", "return z / (1.0 + exp(-z));", "return z / (1.0 + exp(z));"),
+    ("h0_ignored", "h[n] = h0 ? h0[r * N + n] : 0.0;", "h[n] = 0.0;"),
+    ("h0_wrong_row", "h[n] = h0 ? h0[r * N + n] : 0.0;", "h[n] = h0 ? h0[n] : 0.0;"),
+    ("batch_ignored", "const int64_t b = bidx[r];", "const int64_t b = 0;"),
+    ("A_shared_row0", "exp(dlt * A[r * N + n])", "exp(dlt * A[n])"),
+    ("state_reset_each_step", "double acc = 0.0;", "double acc = 0.0; if (t > 0) for (int64_t m = 0; m < N; ++m) h[m] *= 0.5;"),
+    ("h_last_stale", "h_last[r * N + n] = h[n];", "h_last[r * N + n] = h0 ? h0[r * N + n] : 0.0;"),
+    ("delta_from_prev_t", "double v = delta[r * L + t]", "double v = delta[r * L + (t > 0 ? t - 1 : 0)]"),
+    ("C_state_shift", "acc += Cm[(b * N + n) * L + t] * h[n];", "acc += Cm[(b * N + (n + 1) % N) * L + t] * h[n];"),
+    ("last_state_dropped_from_y", "for (int64_t n = 0; n < N; ++n) {\n            const double abar",
+     "for (int64_t n = 0; n < N; ++n) {\n            if (n == N - 1 && N > 1) continue;\n            const double abar"),
+]
+
+
+def _run_pins(lib_path):
+    orc = oracle.Oracle(lib_path)
+    failed = []
+    for pin in P.ALL_PINS:
+        try:
+            pin(orc)
+        except AssertionError as e:
+            failed.append(f"{pin.__name__}: {e}")
+        except (ValueError, FloatingPointError, OverflowError) as e:
+            failed.append(f"{pin.__name__}: raised {type(e).__name__}")
+    return failed
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="needs gcc")
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_mutant(tmp_path, name, old, new):
+    src = open(SRC).read()
+    assert src.count(old) >= 1, f"mutation target for {name} not found: the oracle changed"
+    mutated = src.replace(old, new, 1)
+    path = tmp_path / f"mut_{name}.c"
+    path.write_text(mutated)
+    lib = str(tmp_path / f"libmut_{name}.so")
+    oracle.build(src=str(path), out=lib)
+    failed = _run_pins(lib)
+    assert failed, f"no pin caught the planted mistake {name!r}"
