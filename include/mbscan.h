@@ -1,0 +1,136 @@
+/*
+ * mbscan.h -- C ABI of the MI355X (gfx950) selective-scan library libmbscan.so.
+ *
+ * The operation is the selective state-space scan that every MambaByte layer
+ * runs over its byte sequence (MambaByte, Section 2, eq. (2), with the
+ * discretisation of Appendix D and the output and gating rows of Table 8):
+ *
+ *   dlt_t  = softplus(delta_t + dt_bias)          (eq. (3); or delta_t + dt_bias when delta_softplus == 0)
+ *   h_t[n] = exp(dlt_t A[n]) h_{t-1}[n] + dlt_t B_t[n] u_t    (ZOH on A, simplified Euler on B)
+ *   y_t    = (sum_n C_t[n] h_t[n] + Dskip u_t) * z_t sigmoid(z_t)
+ *
+ * for every (batch b, channel d) row independently, starting from a carried
+ * state h0 and optionally returning the final state: the resume capability
+ * that speculative decoding needs to verify a drafted byte chunk from the
+ * cached state and continue from it (Section 3 "Speculative decoding through
+ * subword drafting"; Appendix G, Algorithm 1).  mb_scan_step is the
+ * one-byte recurrent update used during generation (Section 2: the recurrence
+ * is run directly at inference).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All tensor pointers are DEVICE pointers (memory allocated with hipMalloc or
+ *   by a framework on the GPU that is current for the calling thread), dense
+ *   and row-major in the layouts stated below.  The caller owns every buffer;
+ *   the library keeps no pointer after the call returns.
+ * - Work is enqueued on `stream` (a hipStream_t; NULL means the default
+ *   stream) and the call returns without waiting.  Argument errors are found
+ *   on the host before anything is enqueued and return a negative mb_status;
+ *   a launch failure returns MB_ERR_HIP.  Faults during execution surface at
+ *   the caller's next synchronisation.  The library never prints or aborts.
+ * - Element types: "act" tensors (u, delta, z, B, C and their step
+ *   counterparts) share one type, in_dtype: MB_F32 (IEEE float) or MB_BF16
+ *   (bfloat16).  A, Dskip, dt_bias, h0, h_last and the step state h are
+ *   always float.  The output y has type out_dtype.  All arithmetic is fp32.
+ * - Alignment: every pointer must be aligned to its element size.
+ * - Sizes: batch, dim, seqlen >= 0 (an empty problem is valid and enqueues
+ *   nothing, except that seqlen == 0 still writes h_last = h0, or zeros);
+ *   dstate must be 16 (the n_state of every MambaByte model, Table 9), 8, 4,
+ *   2 or 1; batch * dim * seqlen must stay below 2^62.
+ */
+#ifndef MBSCAN_H
+#define MBSCAN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MB_ABI_VERSION 1
+
+typedef enum {
+    MB_F32 = 0,
+    MB_BF16 = 1
+} mb_dtype;
+
+typedef enum {
+    MB_OK = 0,
+    MB_ERR_NULL = -1,        /* a required pointer is NULL */
+    MB_ERR_SHAPE = -2,       /* a size is negative or too large */
+    MB_ERR_DTYPE = -3,       /* in_dtype or out_dtype is not an mb_dtype */
+    MB_ERR_ALIGN = -4,       /* a pointer is not aligned to its element size */
+    MB_ERR_UNSUPPORTED = -5, /* dstate not in {1, 2, 4, 8, 16}, or a reserved field is set */
+    MB_ERR_HIP = -6,         /* the HIP runtime reported an error when launching */
+    MB_ERR_ALIAS = -7        /* an output overlaps an input it may not overlap */
+} mb_status;
+
+/* Problem description of mb_scan_fwd. */
+typedef struct {
+    int64_t batch;          /* B: independent sequences */
+    int64_t dim;            /* D: channels (e * d in the paper's notation) */
+    int64_t seqlen;         /* L: bytes in the sequence */
+    int64_t dstate;         /* N: SSM state size per channel (n_state) */
+    int32_t in_dtype;       /* mb_dtype of u, delta, z, Bmat, Cmat */
+    int32_t out_dtype;      /* mb_dtype of y */
+    int32_t delta_softplus; /* nonzero: dlt = softplus(delta + dt_bias); zero: dlt = delta + dt_bias */
+    int32_t reserved;       /* must be 0 */
+} mb_scan_desc;
+
+/*
+ * Forward selective scan over a whole sequence (Section 2, eq. (2); the
+ * parallel-scan path of Section 2 "Implementation" that also verifies drafted
+ * bytes in Algorithm 1).
+ *
+ *   u, delta     act   (B, D, L)  input x and the raw timestep, time contiguous
+ *   A            float (D, N)     diagonal of A per channel (normally negative)
+ *   Bmat, Cmat   act   (B, N, L)  input and output projections, shared by all
+ *                                 channels of a batch element, time contiguous
+ *   Dskip        float (D)        skip weight; NULL means 0
+ *   dt_bias      float (D)        added to delta before softplus; NULL means 0
+ *   z            act   (B, D, L)  gate input; NULL means no gate (y = C h + D u)
+ *   h0           float (B, D, N)  initial state; NULL means zeros
+ *   y            out   (B, D, L)  output; must not overlap any input
+ *   h_last       float (B, D, N)  state after the last byte; NULL means not
+ *                                 written.  It may be the same buffer as h0
+ *                                 (each row reads its h0 before writing), but
+ *                                 must not partially overlap it or any other
+ *                                 argument.
+ */
+int mb_scan_fwd(const mb_scan_desc *desc,
+                const void *u, const void *delta, const float *A,
+                const void *Bmat, const void *Cmat,
+                const float *Dskip, const float *dt_bias, const void *z,
+                const float *h0, void *y, float *h_last, void *stream);
+
+/*
+ * One recurrent step per row, the state updated in place (Section 2:
+ * generation runs the recurrence directly; Algorithm 1's byte-level
+ * correction loop).  Identical to mb_scan_fwd with L = 1, h0 = h_last = h.
+ *
+ *   u_t, delta_t   act   (B, D)     this byte's input and raw timestep
+ *   A              float (D, N)
+ *   B_t, C_t       act   (B, N)
+ *   Dskip, dt_bias float (D)        NULL means 0
+ *   z_t            act   (B, D)     NULL means no gate
+ *   h              float (B, D, N)  state, read then overwritten; required
+ *   y_t            out   (B, D)     output; must not overlap any input or h
+ */
+int mb_scan_step(int64_t batch, int64_t dim, int64_t dstate,
+                 int32_t in_dtype, int32_t out_dtype, int32_t delta_softplus,
+                 const void *u_t, const void *delta_t, const float *A,
+                 const void *B_t, const void *C_t,
+                 const float *Dskip, const float *dt_bias, const void *z_t,
+                 float *h, void *y_t, void *stream);
+
+/* Static, NUL-terminated description of a status code (never NULL). */
+const char *mb_status_string(int status);
+
+/* MB_ABI_VERSION of the built library. */
+int mb_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MBSCAN_H */

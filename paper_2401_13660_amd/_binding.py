@@ -1,0 +1,166 @@
+"""Python binding of libmbscan.so: argument marshalling only.
+
+Every step of the scan runs in the HIP kernels behind the C ABI declared in
+``include/mbscan.h``; this module checks torch tensors, allocates outputs with
+torch (device memory and streams are all PyTorch is used for) and passes raw
+device pointers plus the current HIP stream.  There is no fallback: without the
+built library every call raises ``MBScanError``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmbscan.so")
+
+MB_F32, MB_BF16 = 0, 1
+_STATUS_OK = 0
+
+
+class MBScanError(RuntimeError):
+    pass
+
+
+class ScanDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int64), ("dim", ctypes.c_int64), ("seqlen", ctypes.c_int64),
+                ("dstate", ctypes.c_int64), ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
+                ("delta_softplus", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+_lib = None
+_VP = ctypes.c_void_p
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load (once) and return the HIP library; raise loudly if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise MBScanError(f"{path} is not built; run `python -m paper_2401_13660_amd.build` "
+                          "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(path)
+    lib.mb_scan_fwd.restype = ctypes.c_int
+    lib.mb_scan_fwd.argtypes = [ctypes.POINTER(ScanDesc)] + [_VP] * 12
+    lib.mb_scan_step.restype = ctypes.c_int
+    lib.mb_scan_step.argtypes = [ctypes.c_int64] * 3 + [ctypes.c_int32] * 3 + [_VP] * 11
+    lib.mb_status_string.restype = ctypes.c_char_p
+    lib.mb_status_string.argtypes = [ctypes.c_int]
+    lib.mb_abi_version.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(status: int, what: str):
+    if status != _STATUS_OK:
+        msg = load_library().mb_status_string(status).decode()
+        raise MBScanError(f"{what} failed with status {status}: {msg}")
+
+
+def _dt(t: torch.dtype) -> int:
+    if t == torch.float32:
+        return MB_F32
+    if t == torch.bfloat16:
+        return MB_BF16
+    raise MBScanError(f"unsupported element type {t}; use float32 or bfloat16")
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _need(t, name, shape, dtype=None, device=None):
+    if not isinstance(t, torch.Tensor):
+        raise MBScanError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise MBScanError(f"{name} must be a GPU tensor")
+    if device is not None and t.device != device:
+        raise MBScanError(f"{name} is on {t.device}, expected {device}")
+    if tuple(t.shape) != tuple(shape):
+        raise MBScanError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if dtype is not None and t.dtype != dtype:
+        raise MBScanError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise MBScanError(f"{name} must be contiguous")
+
+
+def scan_fwd(u, delta, A, B, C, D=None, dt_bias=None, z=None, h0=None, *, delta_softplus=True,
+             out_dtype=torch.float32, return_last_state=False, out=None, h_last=None):
+    """Selective scan over (batch, dim, L) inputs; returns y or (y, h_last).
+
+    u, delta, z: (batch, dim, L); B, C: (batch, N, L), all of one dtype (fp32 or bf16);
+    A: (dim, N) fp32; D, dt_bias: (dim,) fp32; h0: (batch, dim, N) fp32.
+    """
+    lib = load_library()
+    if not isinstance(u, torch.Tensor) or u.dim() != 3:
+        raise MBScanError("u must be a (batch, dim, L) tensor")
+    nb, dim, L = u.shape
+    if not isinstance(A, torch.Tensor) or A.dim() != 2:
+        raise MBScanError("A must be a (dim, N) tensor")
+    N = A.shape[1]
+    dev, act = u.device, u.dtype
+    _need(u, "u", (nb, dim, L), act, dev)
+    _need(delta, "delta", (nb, dim, L), act, dev)
+    _need(A, "A", (dim, N), torch.float32, dev)
+    _need(B, "B", (nb, N, L), act, dev)
+    _need(C, "C", (nb, N, L), act, dev)
+    if z is not None:
+        _need(z, "z", (nb, dim, L), act, dev)
+    if D is not None:
+        _need(D, "D", (dim,), torch.float32, dev)
+    if dt_bias is not None:
+        _need(dt_bias, "dt_bias", (dim,), torch.float32, dev)
+    if h0 is not None:
+        _need(h0, "h0", (nb, dim, N), torch.float32, dev)
+    if out is None:
+        out = torch.empty((nb, dim, L), dtype=out_dtype, device=dev)
+    else:
+        _need(out, "out", (nb, dim, L), None, dev)
+    if return_last_state and h_last is None:
+        h_last = torch.empty((nb, dim, N), dtype=torch.float32, device=dev)
+    elif h_last is not None:
+        _need(h_last, "h_last", (nb, dim, N), torch.float32, dev)
+    desc = ScanDesc(nb, dim, L, N, _dt(act), _dt(out.dtype), 1 if delta_softplus else 0, 0)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    with torch.cuda.device(dev):
+        st = lib.mb_scan_fwd(ctypes.byref(desc), _ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C),
+                             _ptr(D), _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(out), _ptr(h_last),
+                             stream)
+    _check(st, "mb_scan_fwd")
+    return (out, h_last) if (return_last_state or h_last is not None) else out
+
+
+def scan_step(h, u_t, delta_t, A, B_t, C_t, D=None, dt_bias=None, z_t=None, *, delta_softplus=True,
+              out_dtype=torch.float32, out=None):
+    """One recurrent step; h (batch, dim, N) fp32 is updated in place.  Returns y_t (batch, dim)."""
+    lib = load_library()
+    if not isinstance(h, torch.Tensor) or h.dim() != 3:
+        raise MBScanError("h must be a (batch, dim, N) tensor")
+    nb, dim, N = h.shape
+    dev, act = h.device, u_t.dtype
+    _need(h, "h", (nb, dim, N), torch.float32, dev)
+    _need(u_t, "u_t", (nb, dim), act, dev)
+    _need(delta_t, "delta_t", (nb, dim), act, dev)
+    _need(A, "A", (dim, N), torch.float32, dev)
+    _need(B_t, "B_t", (nb, N), act, dev)
+    _need(C_t, "C_t", (nb, N), act, dev)
+    if z_t is not None:
+        _need(z_t, "z_t", (nb, dim), act, dev)
+    if D is not None:
+        _need(D, "D", (dim,), torch.float32, dev)
+    if dt_bias is not None:
+        _need(dt_bias, "dt_bias", (dim,), torch.float32, dev)
+    if out is None:
+        out = torch.empty((nb, dim), dtype=out_dtype, device=dev)
+    else:
+        _need(out, "out", (nb, dim), None, dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    with torch.cuda.device(dev):
+        st = lib.mb_scan_step(nb, dim, N, _dt(act), _dt(out.dtype), 1 if delta_softplus else 0,
+                              _ptr(u_t), _ptr(delta_t), _ptr(A), _ptr(B_t), _ptr(C_t), _ptr(D),
+                              _ptr(dt_bias), _ptr(z_t), _ptr(h), _ptr(out), stream)
+    _check(st, "mb_scan_step")
+    return out

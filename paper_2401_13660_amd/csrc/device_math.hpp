@@ -1,0 +1,73 @@
+// device_math.hpp -- element formats and fp32 math shared by the gfx950 scan kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mbs {
+
+constexpr float kLog2e = 1.4426950408889634f;  // log2(e)
+constexpr float kLn2 = 0.6931471805599453f;    // ln(2)
+
+// bfloat16 is the upper half of an IEEE float: widening is a shift.
+__device__ __forceinline__ float bf16_lo(uint32_t pair) { return __uint_as_float(pair << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t pair) { return __uint_as_float(pair & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// Round to nearest even (NaN inputs are not expected on this path).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t x = __float_as_uint(f);
+    x += 0x7fffu + ((x >> 16) & 1u);
+    return (uint16_t)(x >> 16);
+}
+
+// Hardware transcendentals: v_exp_f32 = 2^x, v_log_f32 = log2 x, v_rcp_f32 = 1/x.
+__device__ __forceinline__ float hw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float hw_log2(float x) { return __builtin_amdgcn_logf(x); }
+__device__ __forceinline__ float hw_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// softplus(v) = log(1 + e^v), the positivity map of the timestep (eq. (3)).
+// For v > 20 the correction log1p(e^-v) < 2.1e-9 is below half an ulp of v.
+// Otherwise log1p(e) with e = e^v is taken as log(w) with w = fl(1 + e), plus
+// the first-order term c / w of the rounding error c = e - (w - 1) (exact in
+// fp32).  The term only matters for small e, where w is close to 1 and
+// (2 - w) is an accurate stand-in for 1 / w; for w >= 2 it is below 2^-24 of
+// log(w) and is dropped (the clamp keeps (2 - w) from amplifying c).
+__device__ __forceinline__ float softplus_f32(float v) {
+    const float e = hw_exp2(v * kLog2e);
+    const float w = 1.0f + e;
+    const float c = e - (w - 1.0f);
+    const float lg = hw_log2(w) * kLn2;
+    const float sp = __builtin_fmaf(c, __builtin_fmaxf(2.0f - w, 0.0f), lg);
+    return v > 20.0f ? v : sp;
+}
+
+// silu(z) = z * sigmoid(z), the Swish gate (Table 8, Fig. 5).
+__device__ __forceinline__ float silu_f32(float z) {
+    return z * hw_rcp(1.0f + hw_exp2(-z * kLog2e));
+}
+
+template <int DT> struct Act;  // element access by mb_dtype
+
+template <> struct Act<0> {    // MB_F32
+    using T = float;
+    static __device__ __forceinline__ float ld(const void *p, int64_t i) {
+        return static_cast<const float *>(p)[i];
+    }
+};
+template <> struct Act<1> {    // MB_BF16
+    using T = uint16_t;
+    static __device__ __forceinline__ float ld(const void *p, int64_t i) {
+        return bf16_to_f32(static_cast<const uint16_t *>(p)[i]);
+    }
+};
+
+template <int DT> __device__ __forceinline__ void st_out(void *p, int64_t i, float v);
+template <> __device__ __forceinline__ void st_out<0>(void *p, int64_t i, float v) {
+    static_cast<float *>(p)[i] = v;
+}
+template <> __device__ __forceinline__ void st_out<1>(void *p, int64_t i, float v) {
+    static_cast<uint16_t *>(p)[i] = f32_to_bf16(v);
+}
+
+}  // namespace mbs

@@ -1,0 +1,219 @@
+// mbscan.hip -- the C ABI of libmbscan.so: argument checks and kernel dispatch.
+//
+// Every entry point validates its arguments on the host, enqueues its kernels
+// on the caller's stream and returns; see include/mbscan.h for the contract.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "mbscan.h"
+#include "scan_params.hpp"
+#include "scan_rowwise.hpp"
+#include "scan_step.hpp"
+
+namespace {
+
+using mbs::ScanParams;
+using mbs::StepParams;
+
+constexpr int64_t kMaxElems = int64_t(1) << 62;
+
+bool valid_dtype(int32_t t) { return t == MB_F32 || t == MB_BF16; }
+size_t dtype_size(int32_t t) { return t == MB_BF16 ? 2 : 4; }
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Does [a, a+na) overlap [b, b+nb)?  Null or empty ranges never overlap.
+bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
+    if (!a || !b || na == 0 || nb == 0) return false;
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + nb && y < x + na;
+}
+
+// a * b without overflow past kMaxElems (both non-negative).
+bool mul_ok(int64_t a, int64_t b, int64_t *out) {
+    if (a != 0 && b > kMaxElems / a) return false;
+    *out = a * b;
+    return true;
+}
+
+bool supported_dstate(int64_t n) { return n == 1 || n == 2 || n == 4 || n == 8 || n == 16; }
+
+hipError_t launch(const void *fn, dim3 grid, dim3 block, void *params, void *stream) {
+    void *args[] = {params};
+    return hipLaunchKernel(fn, grid, block, args, 0, static_cast<hipStream_t>(stream));
+}
+
+template <int IN, int OUT, int N>
+hipError_t fwd_rowwise(ScanParams &p, void *stream) {
+    const int64_t rows = p.batch * p.dim;
+    const dim3 block(64), grid((unsigned)((rows + 63) / 64));
+    return launch(reinterpret_cast<const void *>(&mbs::scan_fwd_rowwise<IN, OUT, N>), grid, block, &p,
+                  stream);
+}
+
+template <int IN, int OUT>
+hipError_t fwd_dispatch_n(ScanParams &p, int64_t N, void *stream) {
+    switch (N) {
+        case 1: return fwd_rowwise<IN, OUT, 1>(p, stream);
+        case 2: return fwd_rowwise<IN, OUT, 2>(p, stream);
+        case 4: return fwd_rowwise<IN, OUT, 4>(p, stream);
+        case 8: return fwd_rowwise<IN, OUT, 8>(p, stream);
+        default: return fwd_rowwise<IN, OUT, 16>(p, stream);
+    }
+}
+
+template <int IN, int OUT, int N>
+hipError_t step_launch(StepParams &p, void *stream) {
+    constexpr int lanes = N >= 4 ? 4 : 1;
+    const int64_t threads = p.batch * p.dim * lanes;
+    const dim3 block(256), grid((unsigned)((threads + 255) / 256));
+    return launch(reinterpret_cast<const void *>(&mbs::scan_step_kernel<IN, OUT, N>), grid, block, &p,
+                  stream);
+}
+
+template <int IN, int OUT>
+hipError_t step_dispatch_n(StepParams &p, int64_t N, void *stream) {
+    switch (N) {
+        case 1: return step_launch<IN, OUT, 1>(p, stream);
+        case 2: return step_launch<IN, OUT, 2>(p, stream);
+        case 4: return step_launch<IN, OUT, 4>(p, stream);
+        case 8: return step_launch<IN, OUT, 8>(p, stream);
+        default: return step_launch<IN, OUT, 16>(p, stream);
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+int mb_abi_version(void) { return MB_ABI_VERSION; }
+
+const char *mb_status_string(int status) {
+    switch (status) {
+        case MB_OK: return "ok";
+        case MB_ERR_NULL: return "a required pointer is NULL";
+        case MB_ERR_SHAPE: return "a size is negative or too large";
+        case MB_ERR_DTYPE: return "unknown element type";
+        case MB_ERR_ALIGN: return "a pointer is not aligned to its element size";
+        case MB_ERR_UNSUPPORTED: return "unsupported dstate or reserved field set";
+        case MB_ERR_HIP: return "the HIP runtime failed to launch a kernel";
+        case MB_ERR_ALIAS: return "an output overlaps an input";
+        default: return "unknown status";
+    }
+}
+
+int mb_scan_fwd(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
+                const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
+                const void *z, const float *h0, void *y, float *h_last, void *stream) {
+    if (!desc) return MB_ERR_NULL;
+    const int64_t B = desc->batch, D = desc->dim, L = desc->seqlen, N = desc->dstate;
+    if (B < 0 || D < 0 || L < 0 || N < 0) return MB_ERR_SHAPE;
+    if (!valid_dtype(desc->in_dtype) || !valid_dtype(desc->out_dtype)) return MB_ERR_DTYPE;
+    if (desc->reserved != 0 || !supported_dstate(N)) return MB_ERR_UNSUPPORTED;
+    int64_t rows, elems, bc_elems, state_elems;
+    if (!mul_ok(B, D, &rows) || !mul_ok(rows, L, &elems) || !mul_ok(B * N, L, &bc_elems) ||
+        !mul_ok(rows, N, &state_elems))
+        return MB_ERR_SHAPE;
+    if (rows == 0) return MB_OK;
+
+    if (!A) return MB_ERR_NULL;
+    if (L > 0 && (!u || !delta || !Bmat || !Cmat || !y)) return MB_ERR_NULL;
+
+    const size_t in_sz = dtype_size(desc->in_dtype), out_sz = dtype_size(desc->out_dtype);
+    const void *act[] = {u, delta, Bmat, Cmat, z};
+    for (const void *p : act)
+        if (p && !aligned(p, in_sz)) return MB_ERR_ALIGN;
+    const void *f32s[] = {A, Dskip, dt_bias, h0, h_last};
+    for (const void *p : f32s)
+        if (p && !aligned(p, 4)) return MB_ERR_ALIGN;
+    if (y && !aligned(y, out_sz)) return MB_ERR_ALIGN;
+
+    // y may overlap nothing; h_last may only coincide exactly with h0.
+    const size_t act_bytes = (size_t)elems * in_sz, bc_bytes = (size_t)bc_elems * in_sz;
+    const size_t st_bytes = (size_t)state_elems * 4, a_bytes = (size_t)(D * N) * 4, v_bytes = (size_t)D * 4;
+    struct Range { const void *p; size_t n; } ins[] = {
+        {u, act_bytes}, {delta, act_bytes}, {z, act_bytes}, {Bmat, bc_bytes}, {Cmat, bc_bytes},
+        {A, a_bytes}, {Dskip, v_bytes}, {dt_bias, v_bytes}, {h0, st_bytes}};
+    const size_t y_bytes = (size_t)elems * out_sz;
+    for (const Range &r : ins) {
+        if (overlaps(y, y_bytes, r.p, r.n)) return MB_ERR_ALIAS;
+        if (r.p == h0) continue;
+        if (overlaps(h_last, st_bytes, r.p, r.n)) return MB_ERR_ALIAS;
+    }
+    if (overlaps(h_last, st_bytes, y, y_bytes)) return MB_ERR_ALIAS;
+    if (h0 && h_last && h0 != h_last && overlaps(h_last, st_bytes, h0, st_bytes)) return MB_ERR_ALIAS;
+
+    if (L == 0) {
+        if (!h_last || h_last == h0) return MB_OK;
+        struct { const float *h0; float *h_last; int64_t n; } cp{h0, h_last, state_elems};
+        void *args[] = {&cp.h0, &cp.h_last, &cp.n};
+        const dim3 block(256), grid((unsigned)((state_elems + 255) / 256));
+        const hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&mbs::copy_state), grid, block,
+                                             args, 0, static_cast<hipStream_t>(stream));
+        return e == hipSuccess ? MB_OK : MB_ERR_HIP;
+    }
+
+    ScanParams p{};
+    p.batch = B; p.dim = D; p.seqlen = L;
+    p.u = u; p.delta = delta; p.Bm = Bmat; p.Cm = Cmat; p.z = z;
+    p.A = A; p.Dskip = Dskip; p.dt_bias = dt_bias; p.h0 = h0;
+    p.y = y; p.h_last = h_last;
+    p.delta_softplus = desc->delta_softplus ? 1 : 0;
+
+    hipError_t e;
+    if (desc->in_dtype == MB_F32)
+        e = desc->out_dtype == MB_F32 ? fwd_dispatch_n<0, 0>(p, N, stream) : fwd_dispatch_n<0, 1>(p, N, stream);
+    else
+        e = desc->out_dtype == MB_F32 ? fwd_dispatch_n<1, 0>(p, N, stream) : fwd_dispatch_n<1, 1>(p, N, stream);
+    return e == hipSuccess ? MB_OK : MB_ERR_HIP;
+}
+
+int mb_scan_step(int64_t batch, int64_t dim, int64_t dstate, int32_t in_dtype, int32_t out_dtype,
+                 int32_t delta_softplus, const void *u_t, const void *delta_t, const float *A,
+                 const void *B_t, const void *C_t, const float *Dskip, const float *dt_bias,
+                 const void *z_t, float *h, void *y_t, void *stream) {
+    if (batch < 0 || dim < 0 || dstate < 0) return MB_ERR_SHAPE;
+    if (!valid_dtype(in_dtype) || !valid_dtype(out_dtype)) return MB_ERR_DTYPE;
+    if (!supported_dstate(dstate)) return MB_ERR_UNSUPPORTED;
+    int64_t rows, state_elems, bc_elems;
+    if (!mul_ok(batch, dim, &rows) || !mul_ok(rows, dstate, &state_elems) ||
+        !mul_ok(batch, dstate, &bc_elems))
+        return MB_ERR_SHAPE;
+    if (rows == 0) return MB_OK;
+    if (!u_t || !delta_t || !A || !B_t || !C_t || !h || !y_t) return MB_ERR_NULL;
+
+    const size_t in_sz = dtype_size(in_dtype), out_sz = dtype_size(out_dtype);
+    const void *act[] = {u_t, delta_t, B_t, C_t, z_t};
+    for (const void *p : act)
+        if (p && !aligned(p, in_sz)) return MB_ERR_ALIGN;
+    const void *f32s[] = {A, Dskip, dt_bias, h};
+    for (const void *p : f32s)
+        if (p && !aligned(p, 4)) return MB_ERR_ALIGN;
+    if (!aligned(y_t, out_sz)) return MB_ERR_ALIGN;
+
+    const size_t act_bytes = (size_t)rows * in_sz, bc_bytes = (size_t)bc_elems * in_sz;
+    const size_t st_bytes = (size_t)state_elems * 4;
+    struct Range { const void *p; size_t n; } ins[] = {
+        {u_t, act_bytes}, {delta_t, act_bytes}, {z_t, act_bytes}, {B_t, bc_bytes}, {C_t, bc_bytes},
+        {A, (size_t)(dim * dstate) * 4}, {Dskip, (size_t)dim * 4}, {dt_bias, (size_t)dim * 4}};
+    const size_t y_bytes = (size_t)rows * out_sz;
+    for (const Range &r : ins)
+        if (overlaps(y_t, y_bytes, r.p, r.n) || overlaps(h, st_bytes, r.p, r.n)) return MB_ERR_ALIAS;
+    if (overlaps(y_t, y_bytes, h, st_bytes)) return MB_ERR_ALIAS;
+
+    StepParams p{};
+    p.batch = batch; p.dim = dim;
+    p.u = u_t; p.delta = delta_t; p.Bt = B_t; p.Ct = C_t; p.z = z_t;
+    p.A = A; p.Dskip = Dskip; p.dt_bias = dt_bias; p.h = h; p.y = y_t;
+    p.delta_softplus = delta_softplus ? 1 : 0;
+
+    hipError_t e;
+    if (in_dtype == MB_F32)
+        e = out_dtype == MB_F32 ? step_dispatch_n<0, 0>(p, dstate, stream) : step_dispatch_n<0, 1>(p, dstate, stream);
+    else
+        e = out_dtype == MB_F32 ? step_dispatch_n<1, 0>(p, dstate, stream) : step_dispatch_n<1, 1>(p, dstate, stream);
+    return e == hipSuccess ? MB_OK : MB_ERR_HIP;
+}
+
+}  // extern "C"

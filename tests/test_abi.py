@@ -1,0 +1,122 @@
+"""The C ABI on the CPU: the library loads, exports what the header declares,
+and rejects bad arguments before touching the GPU (no compute call is made)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2401_13660_amd as mb
+from paper_2401_13660_amd import _binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mbscan.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(B.LIB_PATH), reason="libmbscan.so not built")
+
+# The argument-error cases hand the library fake device addresses.  Each case
+# is invalid, so validation rejects it before any launch; as a second guard
+# they only run where no GPU driver is present (the CPU suite), never on a GPU.
+no_gpu_only = pytest.mark.skipif(os.path.exists("/dev/kfd"),
+                                 reason="fake-pointer error paths run only on a machine without a GPU")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mb_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    lib = mb.load_library()
+    names = declared_functions()
+    assert {"mb_scan_fwd", "mb_scan_step", "mb_status_string", "mb_abi_version"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in mbscan.h but not exported"
+
+
+def test_version_and_status_strings():
+    lib = mb.load_library()
+    assert lib.mb_abi_version() == 1
+    for code in range(-7, 1):
+        assert lib.mb_status_string(code)
+    assert lib.mb_status_string(-99) == b"unknown status"
+
+
+def _desc(**kw):
+    d = dict(batch=2, dim=8, seqlen=16, dstate=16, in_dtype=1, out_dtype=0, delta_softplus=1, reserved=0)
+    d.update(kw)
+    return B.ScanDesc(**d)
+
+
+# Fake, distinct, well-aligned "device" addresses: every call below must fail
+# validation, so none of them is ever dereferenced.
+P = {k: 0x10000000 * (i + 1) for i, k in enumerate(
+    ["u", "delta", "A", "B", "C", "D", "bias", "z", "h0", "y", "hl"])}
+
+
+def _fwd(desc, **over):
+    a = dict(P)
+    a.update(over)
+    lib = mb.load_library()
+    return lib.mb_scan_fwd(ctypes.byref(desc) if desc is not None else None, a["u"], a["delta"], a["A"],
+                           a["B"], a["C"], a["D"], a["bias"], a["z"], a["h0"], a["y"], a["hl"], None)
+
+
+@no_gpu_only
+@pytest.mark.parametrize("desc,over,code", [
+    (None, {}, -1),
+    (_desc(batch=-1), {}, -2),
+    (_desc(seqlen=-5), {}, -2),
+    (_desc(batch=1 << 40, dim=1 << 20, seqlen=1 << 10), {}, -2),
+    (_desc(in_dtype=7), {}, -3),
+    (_desc(out_dtype=-1), {}, -3),
+    (_desc(dstate=3), {}, -5),
+    (_desc(dstate=32), {}, -5),
+    (_desc(reserved=1), {}, -5),
+    (_desc(), dict(u=None), -1),
+    (_desc(), dict(A=None), -1),
+    (_desc(), dict(y=None), -1),
+    (_desc(), dict(B=None), -1),
+    (_desc(), dict(u=P["u"] + 1), -4),                  # bf16 needs 2-byte alignment
+    (_desc(in_dtype=0), dict(delta=P["delta"] + 2), -4),  # fp32 needs 4-byte alignment
+    (_desc(), dict(hl=P["hl"] + 2), -4),
+    (_desc(), dict(y=P["u"] + 64), -7),                  # y inside u
+    (_desc(), dict(hl=P["z"]), -7),                      # h_last on top of z
+    (_desc(), dict(hl=P["h0"] + 64), -7),                # h_last partially over h0
+])
+def test_fwd_rejects(desc, over, code):
+    assert _fwd(desc, **over) == code
+
+
+@no_gpu_only
+def test_fwd_empty_problem_is_ok_and_launches_nothing():
+    assert _fwd(_desc(batch=0)) == 0
+    assert _fwd(_desc(dim=0), u=None, delta=None, A=None) == 0
+
+
+@no_gpu_only
+def test_step_rejects():
+    lib = mb.load_library()
+    f = lib.mb_scan_step
+    ok = [P["u"], P["delta"], P["A"], P["B"], P["C"], P["D"], P["bias"], P["z"], P["h0"], P["y"], None]
+    assert f(-1, 8, 16, 1, 0, 1, *ok) == -2
+    assert f(2, 8, 12, 1, 0, 1, *ok) == -5
+    assert f(2, 8, 16, 4, 0, 1, *ok) == -3
+    bad = list(ok); bad[8] = None                       # h is required
+    assert f(2, 8, 16, 1, 0, 1, *bad) == -1
+    bad = list(ok); bad[9] = P["u"]                     # y_t on top of u_t
+    assert f(2, 8, 16, 1, 0, 1, *bad) == -7
+    bad = list(ok); bad[8] = P["A"]                     # h on top of A
+    assert f(2, 8, 16, 1, 0, 1, *bad) == -7
+    assert f(0, 8, 16, 1, 0, 1, *ok) == 0
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    saved = B._lib
+    try:
+        B._lib = None
+        with pytest.raises(B.MBScanError):
+            B.load_library(str(tmp_path / "missing.so"))
+    finally:
+        B._lib = saved
