@@ -1,0 +1,176 @@
+#!/usr/bin/env python3
+"""Benchmark of the selective scan on one MI355X.
+
+One step = one mb_scan_fwd over the MambaByte-972M layer shape (batch 4,
+L = 8,192 bytes, dim 3,584, N = 16; bf16 activations, fp32 output and state,
+z-gated) with inputs already resident in HBM.  Prints one JSON line with the
+whole-job throughput (algorithmic GB/s), B*L*D elements/s, the HBM roofline of
+the scan kernel and the fp64 CPU oracle timed on this host's cores over the
+same workload (which doubles as the parity gate).
+
+    python bench.py [--gpus 1] [--steps 50] [--warmup 10] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
+METRIC = "selective-scan GB/s & %HBM peak (972M layer, L=8192); B·L·D elems/s"
+DEFAULT_WORKLOAD = "mambabyte972m_L8192"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def algorithmic_bytes(inp, out_bytes=4, want_h_last=False) -> int:
+    """Each input read once and each output written once (the roofline's bytes)."""
+    act = 2 if inp.dtype == "bf16" else 4
+    E = inp.batch * inp.dim * inp.seqlen
+    n_act = 2 + (1 if inp.z is not None else 0)                  # u, delta (, z)
+    b = E * (n_act * act + out_bytes)
+    b += 2 * inp.batch * inp.dstate * inp.seqlen * act            # B, C
+    b += inp.dim * inp.dstate * 4                                 # A
+    b += inp.dim * 4 * ((inp.Dskip is not None) + (inp.dt_bias is not None))
+    state = inp.batch * inp.dim * inp.dstate * 4
+    b += state * ((inp.h0 is not None) + bool(want_h_last))
+    return int(b)
+
+
+def kernel_sources_digest() -> str:
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2401_13660_amd", "csrc", "*"))):
+        with open(p, "rb") as f:
+            h.update(os.path.basename(p).encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 PMC summary, if it was
+    taken on the current kernel sources (else None)."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f).get(workload)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("kernel_sources") != kernel_sources_digest():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(inp, y_gpu):
+    """fp64 oracle on this host's cores over the whole workload, batch by batch;
+    also the parity gate for the GPU output of the same inputs."""
+    import oracle
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from parity import TOL_Y, rel_err
+
+    orc = oracle.default()
+    threads = orc.max_threads()
+    elapsed = 0.0
+    worst = 0.0
+    for b in range(inp.batch):
+        rows = np.arange(b * inp.dim, (b + 1) * inp.dim)
+        t0 = time.perf_counter()
+        y_ref, _ = oracle.scan_inputs(inp, rows=rows)
+        elapsed += time.perf_counter() - t0
+        yg = y_gpu[b].float().cpu().numpy().astype(np.float64)
+        worst = max(worst, rel_err(yg, y_ref))
+    E = inp.batch * inp.dim * inp.seqlen
+    return dict(elapsed=elapsed, elems_per_s=E / elapsed, threads=threads, y_err=worst,
+                parity_ok=worst <= TOL_Y)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2401_13660_amd as mb
+    from paper_2401_13660_amd.inputs import WORKLOADS, workload
+
+    inp = workload(args.workload, seed=0)
+    dev = torch.device("cuda:0")
+
+    def t(a):
+        if a is None:
+            return None
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    want_h_last = inp.h0 is not None or args.workload == "mambabyte1p6b_L65536"
+    g = {k: t(v) for k, v in inp.arrays().items()}
+    y = torch.empty((inp.batch, inp.dim, inp.seqlen), dtype=torch.float32, device=dev)
+    h_last = torch.empty((inp.batch, inp.dim, inp.dstate), dtype=torch.float32, device=dev) if want_h_last else None
+
+    def step():
+        mb.scan_fwd(g["u"], g["delta"], g["A"], g["B"], g["C"], D=g.get("Dskip"), dt_bias=g.get("dt_bias"),
+                    z=g.get("z"), h0=g.get("h0"), out=y, h_last=h_last)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+
+    E = inp.batch * inp.dim * inp.seqlen
+    nbytes = algorithmic_bytes(inp, 4, want_h_last)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    traffic = measured_traffic(args.workload)
+
+    line = {
+        "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, **{k: v for k, v in WORKLOADS[args.workload].items()},
+                   "gated": inp.z is not None, "h0": inp.h0 is not None, "h_last": want_h_last,
+                   "out_dtype": "f32", "parallelism": "single GPU"},
+        "elems_per_s": round(E / (ms * 1e-3), 1),
+        "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "algorithmic_bytes": nbytes},
+    }
+    if not args.no_cpu_baseline:
+        cb = cpu_baseline(inp, y)
+        line["cpu_baseline"] = {
+            "value": round(cb["elems_per_s"] * nbytes / E / 1e9, 3), "unit": "GB/s",
+            "elems_per_s": round(cb["elems_per_s"], 1), "cores": cb["threads"], "kind": "oracle",
+            "sample": f"whole workload: {inp.batch} x {inp.dim} rows of L={inp.seqlen}, fp64, "
+                      f"{cb['elapsed']:.1f} s",
+        }
+        line["parity"] = {"y_rel_err_vs_oracle": cb["y_err"], "ok": cb["parity_ok"]}
+        if not cb["parity_ok"]:
+            print(json.dumps(line))
+            print("parity gate failed: GPU output disagrees with the oracle", file=sys.stderr)
+            sys.exit(1)
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

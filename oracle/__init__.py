@@ -58,10 +58,14 @@ class Oracle:
         self.lib.mbo_scan_rows.argtypes = [
             ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
             _D, _D, _D, _D, _D, _D, _D, _I64, ctypes.c_int64, _D, _D, _D, _D]
+        self.lib.mbo_max_threads.restype = ctypes.c_int
         self.lib.mbo_scan_step.restype = ctypes.c_int
         self.lib.mbo_scan_step.argtypes = [
             ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
             _D, _D, _D, _D, _D, _D, _I64, ctypes.c_int64, _D, _D, _D, _D]
+
+    def max_threads(self) -> int:
+        return int(self.lib.mbo_max_threads())
 
     # -- rows ---------------------------------------------------------------
     def scan_rows(self, u, delta, A, Bm, Cm, bidx, *, z=None, Dskip=None, dt_bias=None,

@@ -39,6 +39,9 @@
 #include <stddef.h>
 #include <stdint.h>
 #include <stdlib.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #define MBO_MAX_N 256
 
@@ -160,4 +163,14 @@ int mbo_scan_step(int64_t R, int64_t N, int delta_softplus,
                      h, bidx, B_t, C_t, y_t, h);
     }
     return MBO_OK;
+}
+
+/* Threads the row loop runs on (reported next to the oracle's timing). */
+int mbo_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
 }

@@ -10,6 +10,7 @@
 #include "scan_params.hpp"
 #include "scan_rowwise.hpp"
 #include "scan_step.hpp"
+#include "scan_tiled.hpp"
 
 namespace {
 
@@ -52,8 +53,34 @@ hipError_t fwd_rowwise(ScanParams &p, void *stream) {
                   stream);
 }
 
+template <int IN, int OUT, bool GATE>
+hipError_t fwd_tiled(ScanParams &p, void *stream) {
+    namespace T = mbs::tiled;
+    const void *fn = p.delta_softplus ? reinterpret_cast<const void *>(&T::scan_fwd_tiled<IN, OUT, GATE, true>)
+                                      : reinterpret_cast<const void *>(&T::scan_fwd_tiled<IN, OUT, GATE, false>);
+    const int64_t n_cg = (p.dim + T::kCh - 1) / T::kCh;
+    int64_t seg_len = p.seqlen;
+    const int64_t waves = n_cg * p.batch;
+    const int64_t blocks = (waves + T::kWavesPerGroup - 1) / T::kWavesPerGroup;
+    void *args[] = {&p, &seg_len};
+    return hipLaunchKernel(fn, dim3((unsigned)blocks), dim3(T::kThreads), args,
+                           sizeof(T::WaveSmem) * T::kWavesPerGroup, static_cast<hipStream_t>(stream));
+}
+
+// The tiled kernel takes dstate 16 with 16-byte aligned activation rows.
+bool tiled_ok(const ScanParams &p, int64_t N, int32_t in_dtype, int32_t out_dtype) {
+    if (N != 16 || p.seqlen % 16 != 0) return false;
+    const void *ptrs[] = {p.u, p.delta, p.z, p.Bm, p.Cm, p.y};
+    for (const void *q : ptrs)
+        if (q && !aligned(q, 16)) return false;
+    (void)in_dtype; (void)out_dtype;
+    return p.batch * ((p.dim + 7) / 8) < (int64_t(1) << 33);
+}
+
 template <int IN, int OUT>
 hipError_t fwd_dispatch_n(ScanParams &p, int64_t N, void *stream) {
+    if (tiled_ok(p, N, IN, OUT))
+        return p.z ? fwd_tiled<IN, OUT, true>(p, stream) : fwd_tiled<IN, OUT, false>(p, stream);
     switch (N) {
         case 1: return fwd_rowwise<IN, OUT, 1>(p, stream);
         case 2: return fwd_rowwise<IN, OUT, 2>(p, stream);

@@ -1,0 +1,265 @@
+// scan_tiled.hpp -- the forward selective scan for dstate = 16, tiled for gfx950.
+//
+// Each wavefront works alone (no workgroup barrier anywhere): it owns 8
+// channels of one batch element over one time segment, and lane l = 8 j + q
+// holds channel j's states 2q and 2q+1 of eq. (2) in VGPRs.  Time advances in
+// chunks of T = 32 bytes; per chunk the wave
+//
+//   A  does the per-element work once: lane (j, q) widens u, delta and z of
+//      channel j at timesteps 4q .. 4q+3 (eight lanes read 64 contiguous bytes
+//      of a row), computes dlt = softplus(delta + dt_bias) (eq. (3)),
+//      dx = dlt * u and silu(z) (Table 8), and publishes (dlt, dx) in its
+//      private LDS area; the wave also stages the chunk's B and C rows there,
+//      time-major and widened to fp32;
+//   B  runs the recurrence for its two states over the 32 timesteps --
+//      abar = 2^(dlt A log2 e) (zero-order hold on A), h = abar h + dx B
+//      (simplified Euler on B) -- reading the next four timesteps' operands
+//      from LDS while computing the current four, and publishes its partial
+//      contraction C_t[2q] h_t[2q] + C_t[2q+1] h_t[2q+1] per timestep;
+//   C  lane (j, q) sums the eight partials of channel j at its own timesteps
+//      4q .. 4q+3, adds Dskip * u, applies the gate and stores y (eight lanes
+//      write 128 contiguous bytes of a row).
+//
+// Global loads run two chunks ahead.  Arithmetic is fp32; the state never
+// leaves VGPRs except through h0 / h_last.  Requires seqlen % 16 == 0 and
+// 16-byte aligned activation rows (the host checks; otherwise it uses the
+// row-per-thread kernel).
+#pragma once
+
+#include "device_math.hpp"
+#include "scan_params.hpp"
+
+#include <type_traits>
+
+namespace mbs {
+namespace tiled {
+
+constexpr int kN = 16;                // states per channel
+constexpr int kCh = 8;                // channels per wave
+constexpr int kQ = 8;                 // state pairs per channel (lanes per channel)
+constexpr int kT = 32;                // timesteps per chunk
+constexpr int kWavesPerGroup = 4;     // independent waves per workgroup
+constexpr int kThreads = kWavesPerGroup * 64;
+
+// 4 consecutive activations of one row (8 bytes bf16, 16 bytes fp32).
+template <int IN> struct Raw4;
+template <> struct Raw4<1> {
+    u32x2 v;
+    __device__ __forceinline__ void load(const void *base, int64_t off) {
+        v = *reinterpret_cast<const u32x2 *>(static_cast<const uint16_t *>(base) + off);
+    }
+    __device__ __forceinline__ void zero() { v = u32x2{0, 0}; }
+    __device__ __forceinline__ float get(int i) const {
+        const uint32_t w = (i >> 1) ? v.y : v.x;
+        return (i & 1) ? bf16_hi(w) : bf16_lo(w);
+    }
+};
+template <> struct Raw4<0> {
+    f32x4 v;
+    __device__ __forceinline__ void load(const void *base, int64_t off) {
+        v = *reinterpret_cast<const f32x4 *>(static_cast<const float *>(base) + off);
+    }
+    __device__ __forceinline__ void zero() { v = f32x4{0, 0, 0, 0}; }
+    __device__ __forceinline__ float get(int i) const { return v[i]; }
+};
+
+// Private LDS area of one wave.
+struct WaveSmem {
+    f32x4 dd[kT / 2][kCh];        // (dlt_t, dx_t, dlt_t+1, dx_t+1), channel j in slot j ^ (row & 7)  2 KB
+    f32x4 bc[kT][kQ];             // (B[2q], B[2q+1], C[2q], C[2q+1]) per timestep        4 KB
+    f32x4 part[kT / 4][kCh][kQ];  // partial outputs, 4 timesteps each, slot q ^ (t / 4)  8 KB
+};
+
+template <int IN, int OUT, bool GATE, bool SOFTPLUS>
+__global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    const int wave = threadIdx.x >> 6;
+    WaveSmem &sm = reinterpret_cast<WaveSmem *>(smem_raw)[wave];
+
+    const int lane = threadIdx.x & 63;
+    const int j = lane >> 3;          // channel within the wave
+    const int q = lane & 7;           // state pair; also the timestep quad of phases A and C
+    const int64_t n_cg = (p.dim + kCh - 1) / kCh;
+    const int64_t nseg = (p.seqlen + seg_len - 1) / seg_len;
+    const int64_t wid = (int64_t)blockIdx.x * kWavesPerGroup + wave;
+    if (wid >= n_cg * p.batch * nseg) return;           // whole wave leaves together
+    const int64_t cg = wid % n_cg;
+    const int64_t b = (wid / n_cg) % p.batch;
+    const int64_t seg = wid / (n_cg * p.batch);
+    const int64_t t_begin = seg * seg_len;
+    const int64_t t_end = t_begin + seg_len < p.seqlen ? t_begin + seg_len : p.seqlen;
+
+    const int64_t d = cg * kCh + j;
+    const bool live = d < p.dim;
+    const int64_t dcl = live ? d : p.dim - 1;           // dead lanes read a valid row, never store
+    const int64_t row = b * p.dim + dcl;
+    const int64_t L = p.seqlen;
+    const int n0 = 2 * q;
+
+    float a2[2], h[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        a2[s] = p.A[dcl * kN + n0 + s] * kLog2e;
+        h[s] = p.h0 ? p.h0[row * kN + n0 + s] : 0.0f;
+    }
+    const float dskip = p.Dskip ? p.Dskip[dcl] : 0.0f;
+    const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
+
+    // B/C staging: lane (tb = l / 8, q) moves timesteps 4 tb .. 4 tb + 3 of
+    // state rows 2q and 2q+1 of B and C, i.e. the four entries bc[4 tb + i][q].
+    const int st_t = (lane >> 3) * 4;
+    const int64_t st_row = (b * kN + 2 * q) * L;
+
+    struct Slot { Raw4<IN> u, dl, z, B0, B1, C0, C1; };
+    Slot s0, s1;
+    // Loads never branch: a chunk past the end of the segment reads the last
+    // valid quad again (those values are never consumed), so the prefetch
+    // registers are written in place every time.
+    auto issue_loads = [&](Slot &sl, int64_t t0) {
+        const int64_t ts = t0 + 4 * q < t_end - 4 ? t0 + 4 * q : t_end - 4;
+        sl.u.load(p.u, row * L + ts);
+        sl.dl.load(p.delta, row * L + ts);
+        if (GATE) sl.z.load(p.z, row * L + ts);
+        const int64_t tb = t0 + st_t < t_end - 4 ? t0 + st_t : t_end - 4;
+        sl.B0.load(p.Bm, st_row + tb);
+        sl.B1.load(p.Bm, st_row + L + tb);
+        sl.C0.load(p.Cm, st_row + tb);
+        sl.C1.load(p.Cm, st_row + L + tb);
+    };
+
+    // Phase B step TQ: timesteps 4 TQ .. 4 TQ + 3, operands already in registers.
+    auto recur4 = [&](const f32x4 (&ddv)[2], const f32x4 (&bcv)[4], auto tq_c) {
+        constexpr int TQ = decltype(tq_c)::value;
+        float acc4[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const float dl = (k & 1) ? ddv[k >> 1].z : ddv[k >> 1].x;
+            const float dx = (k & 1) ? ddv[k >> 1].w : ddv[k >> 1].y;
+            const float a0 = hw_exp2(dl * a2[0]);
+            const float a1 = hw_exp2(dl * a2[1]);
+            h[0] = __builtin_fmaf(a0, h[0], dx * bcv[k][0]);
+            h[1] = __builtin_fmaf(a1, h[1], dx * bcv[k][1]);
+            acc4[k] = __builtin_fmaf(bcv[k][3], h[1], bcv[k][2] * h[0]);
+        }
+        sm.part[TQ][j][q ^ TQ] = f32x4{acc4[0], acc4[1], acc4[2], acc4[3]};
+    };
+    auto load4 = [&](f32x4 (&ddv)[2], f32x4 (&bcv)[4], auto tq_c) {
+        constexpr int TQ = decltype(tq_c)::value;
+#pragma unroll
+        for (int k = 0; k < 2; ++k) ddv[k] = sm.dd[2 * TQ + k][j ^ ((2 * TQ + k) & 7)];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) bcv[k] = sm.bc[4 * TQ + k][q];
+    };
+    // Order this wave's LDS writes before its later reads of other lanes' data.
+    auto wave_sync = [] {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+
+    auto chunk = [&](Slot &sl, int64_t t0) {
+        const int nt = (int)(t_end - t0 < kT ? t_end - t0 : kT);   // valid timesteps, multiple of 16
+
+        // ---- A: per-element work of timesteps 4q .. 4q+3 and B/C staging ------
+        float xs[4], gs[4];
+        {
+            float dl[4], dx[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float x = sl.u.get(k);
+                const float v = sl.dl.get(k) + bias;
+                dl[k] = SOFTPLUS ? softplus_f32(v) : v;
+                dx[k] = dl[k] * x;
+                xs[k] = x;
+                if (GATE) gs[k] = silu_f32(sl.z.get(k));
+            }
+            sm.dd[2 * q][j ^ ((2 * q) & 7)] = f32x4{dl[0], dx[0], dl[1], dx[1]};
+            sm.dd[2 * q + 1][j ^ ((2 * q + 1) & 7)] = f32x4{dl[2], dx[2], dl[3], dx[3]};
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            sm.bc[st_t + k][q] = f32x4{sl.B0.get(k), sl.B1.get(k), sl.C0.get(k), sl.C1.get(k)};
+        wave_sync();
+
+        // refill this slot with the chunk after next while the recurrence runs
+        issue_loads(sl, t0 + 2 * kT);
+
+        // ---- B: the recurrence, fully unrolled over the chunk; the operands of
+        //      step i + 1 are read from LDS while step i computes ----------------
+        {
+            f32x4 ddA[2], bcA[4], ddB[2], bcB[4];
+            using I0 = std::integral_constant<int, 0>;
+            using I1 = std::integral_constant<int, 1>;
+            using I2 = std::integral_constant<int, 2>;
+            using I3 = std::integral_constant<int, 3>;
+            using I4 = std::integral_constant<int, 4>;
+            using I5 = std::integral_constant<int, 5>;
+            using I6 = std::integral_constant<int, 6>;
+            using I7 = std::integral_constant<int, 7>;
+            load4(ddA, bcA, I0{});
+            load4(ddB, bcB, I1{});
+            recur4(ddA, bcA, I0{});
+            load4(ddA, bcA, I2{});
+            recur4(ddB, bcB, I1{});
+            load4(ddB, bcB, I3{});
+            recur4(ddA, bcA, I2{});
+            if (nt == kT) {
+                load4(ddA, bcA, I4{});
+                recur4(ddB, bcB, I3{});
+                load4(ddB, bcB, I5{});
+                recur4(ddA, bcA, I4{});
+                load4(ddA, bcA, I6{});
+                recur4(ddB, bcB, I5{});
+                load4(ddB, bcB, I7{});
+                recur4(ddA, bcA, I6{});
+                recur4(ddB, bcB, I7{});
+            } else {                                // nt == 16: the last, half chunk
+                recur4(ddB, bcB, I3{});
+            }
+        }
+        wave_sync();
+
+        // ---- C: sum the 8 partials of channel j at timesteps 4q .. 4q+3 --------
+        if (4 * q < nt) {
+            f32x4 acc = sm.part[q][j][0 ^ q];
+#pragma unroll
+            for (int w = 1; w < kQ; ++w) acc += sm.part[q][j][w ^ q];
+            float yv[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                float y = __builtin_fmaf(dskip, xs[k], acc[k]);
+                if (GATE) y *= gs[k];
+                yv[k] = y;
+            }
+            if (live) {
+                const int64_t off = row * L + t0 + 4 * q;
+                if (OUT == 0) {
+                    *reinterpret_cast<f32x4 *>(static_cast<float *>(p.y) + off) = f32x4{yv[0], yv[1], yv[2], yv[3]};
+                } else {
+                    const uint32_t w0 = (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
+                    const uint32_t w1 = (uint32_t)f32_to_bf16(yv[2]) | ((uint32_t)f32_to_bf16(yv[3]) << 16);
+                    *reinterpret_cast<u32x2 *>(static_cast<uint16_t *>(p.y) + off) = u32x2{w0, w1};
+                }
+            }
+        }
+        wave_sync();   // part / dd / bc are rewritten by the next chunk
+    };
+
+    issue_loads(s0, t_begin);
+    issue_loads(s1, t_begin + kT);
+    int64_t t0 = t_begin;
+    for (; t0 + 2 * kT <= t_end; t0 += 2 * kT) {   // pairs of full chunks
+        chunk(s0, t0);
+        chunk(s1, t0 + kT);
+    }
+    if (t0 < t_end) chunk(s0, t0);                  // a full chunk and/or a half chunk remain
+    if (t0 + kT < t_end) chunk(s1, t0 + kT);
+
+    if (p.h_last && live) {
+#pragma unroll
+        for (int s = 0; s < 2; ++s) p.h_last[row * kN + n0 + s] = h[s];
+    }
+}
+
+}  // namespace tiled
+}  // namespace mbs
