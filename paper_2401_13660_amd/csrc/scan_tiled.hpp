@@ -81,7 +81,13 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     const int q = lane & 7;           // state pair; also the timestep quad of phases A and C
     const int64_t n_cg = (p.dim + kCh - 1) / kCh;
     const int64_t nseg = (p.seqlen + seg_len - 1) / seg_len;
-    const int64_t wid = (int64_t)blockIdx.x * kWavesPerGroup + wave;
+    // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2);
+    // renumber them so that an XCD works on a contiguous range of (batch,
+    // channel) groups and the B/C rows of a batch stay in one or two L2s.
+    const int64_t per_xcd = (int64_t)gridDim.x / 8;
+    const int64_t k = blockIdx.x;
+    const int64_t lwg = k < per_xcd * 8 ? (k % 8) * per_xcd + k / 8 : k;
+    const int64_t wid = lwg * kWavesPerGroup + wave;
     if (wid >= n_cg * p.batch * nseg) return;           // whole wave leaves together
     const int64_t cg = wid % n_cg;
     const int64_t b = (wid / n_cg) % p.batch;
