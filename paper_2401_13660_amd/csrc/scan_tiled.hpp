@@ -45,8 +45,8 @@ constexpr int kThreads = kWavesPerGroup * 64;
 template <int IN> struct Raw4;
 template <> struct Raw4<1> {
     u32x2 v;
-    __device__ __forceinline__ void load(const void *base, int64_t off) {
-        v = *reinterpret_cast<const u32x2 *>(static_cast<const uint16_t *>(base) + off);
+    __device__ __forceinline__ void load(const void *base, uint32_t off) {
+        v = *reinterpret_cast<const u32x2 *>(static_cast<const char *>(base) + off * 2u);
     }
     __device__ __forceinline__ void zero() { v = u32x2{0, 0}; }
     __device__ __forceinline__ float get(int i) const {
@@ -56,24 +56,39 @@ template <> struct Raw4<1> {
 };
 template <> struct Raw4<0> {
     f32x4 v;
-    __device__ __forceinline__ void load(const void *base, int64_t off) {
-        v = *reinterpret_cast<const f32x4 *>(static_cast<const float *>(base) + off);
+    __device__ __forceinline__ void load(const void *base, uint32_t off) {
+        v = *reinterpret_cast<const f32x4 *>(static_cast<const char *>(base) + off * 4u);
     }
     __device__ __forceinline__ void zero() { v = f32x4{0, 0, 0, 0}; }
     __device__ __forceinline__ float get(int i) const { return v[i]; }
 };
 
-// Private LDS area of one wave.
+// Private LDS area of one wave.  Rows are padded so that both the writes and
+// the reads of every table touch distinct banks (16-byte entries, 64 banks):
+//   dd    row r = timesteps 2r, 2r+1; entry j = (dlt, dx, dlt, dx) of channel j
+//   bc    row t; entry q = (B[2q], B[2q+1], C[2q], C[2q+1]) at timestep t
+//   part  row 8 j + tq = channel j, timesteps 4 tq .. 4 tq + 3; entry q = the
+//         partial output of state pair q at those four timesteps
+constexpr int kDdRow = 9;       // 16-byte entries per row: 8 used + 1 pad
+constexpr int kBcRow = 10;      // 8 used + 2 pad
+constexpr int kPartRow = 9;     // 8 used + 1 pad
 struct WaveSmem {
-    f32x4 dd[kT / 2][kCh];        // (dlt_t, dx_t, dlt_t+1, dx_t+1), channel j in slot j ^ (row & 7)  2 KB
-    f32x4 bc[kT][kQ];             // (B[2q], B[2q+1], C[2q], C[2q+1]) per timestep        4 KB
-    f32x4 part[kT / 4][kCh][kQ];  // partial outputs, 4 timesteps each, slot q ^ (t / 4)  8 KB
+    f32x4 dd[kT / 2][kDdRow];                 // 2.25 KB
+    f32x4 bc[kT][kBcRow];                     // 5 KB
+    f32x4 part[kCh * (kT / 4)][kPartRow];     // 9 KB
 };
 
-template <int IN, int OUT, bool GATE, bool SOFTPLUS>
-__global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len) {
+// PREPASS = false: the scan itself.  With several time segments, the wave of
+//   segment s starts from h0 folded with the aggregates of segments 0..s-1.
+// PREPASS = true: for every segment but the last, the segment's aggregate from a
+//   zero state: P[n] = prod_t abar_t[n] = 2^(A[n] log2e sum_t dlt_t) and the local
+//   end state H[n]; written to carry[((seg * rows + row) * 16 + n) * 2 + {0, 1}].
+//   Folding h <- P h + H is the associative operator of the parallel-scan
+//   formulation (Section 2, "Implementation") applied across segments.
+template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool PREPASS>
+__global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len, float *carry) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     WaveSmem &sm = reinterpret_cast<WaveSmem *>(smem_raw)[wave];
 
     const int lane = threadIdx.x & 63;
@@ -88,7 +103,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     const int64_t k = blockIdx.x;
     const int64_t lwg = k < per_xcd * 8 ? (k % 8) * per_xcd + k / 8 : k;
     const int64_t wid = lwg * kWavesPerGroup + wave;
-    if (wid >= n_cg * p.batch * nseg) return;           // whole wave leaves together
+    if (wid >= n_cg * p.batch * (PREPASS ? nseg - 1 : nseg)) return;   // whole wave leaves together
     const int64_t cg = wid % n_cg;
     const int64_t b = (wid / n_cg) % p.batch;
     const int64_t seg = wid / (n_cg * p.batch);
@@ -102,38 +117,68 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     const int64_t L = p.seqlen;
     const int n0 = 2 * q;
 
+    const int64_t rows = p.batch * p.dim;
     float a2[2], h[2];
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
         a2[s] = p.A[dcl * kN + n0 + s] * kLog2e;
-        h[s] = p.h0 ? p.h0[row * kN + n0 + s] : 0.0f;
+        h[s] = (!PREPASS && p.h0) ? p.h0[row * kN + n0 + s] : 0.0f;
     }
+    if (!PREPASS) {
+        // carry-in: fold the aggregates of the earlier segments into h0
+        for (int64_t s2 = 0; s2 < seg; ++s2) {
+            const f32x4 ph = *reinterpret_cast<const f32x4 *>(carry + ((s2 * rows + row) * kN + n0) * 2);
+            h[0] = __builtin_fmaf(ph.x, h[0], ph.y);
+            h[1] = __builtin_fmaf(ph.z, h[1], ph.w);
+        }
+    }
+    float dsum = 0.0f;                                  // sum of dlt over the segment (PREPASS)
     const float dskip = p.Dskip ? p.Dskip[dcl] : 0.0f;
     const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
 
-    // B/C staging: lane (tb = l / 8, q) moves timesteps 4 tb .. 4 tb + 3 of
-    // state rows 2q and 2q+1 of B and C, i.e. the four entries bc[4 tb + i][q].
-    const int st_t = (lane >> 3) * 4;
-    const int64_t st_row = (b * kN + 2 * q) * L;
+    // Global addressing: wave-uniform 64-bit bases (the wave's first channel
+    // row, or state row 0 of B and C, at the segment start) plus 32-bit lane
+    // offsets in elements, so the loads use the scalar-base form.
+    constexpr int kEl = IN == 1 ? 2 : 4;
+    const int64_t row0 = b * p.dim + cg * kCh;                       // wave-uniform
+    const int64_t act0 = row0 * L + t_begin;
+    const int64_t bc0 = b * kN * L + t_begin;
+    const char *ub = static_cast<const char *>(p.u) + act0 * kEl;
+    const char *db = static_cast<const char *>(p.delta) + act0 * kEl;
+    const char *zb = GATE ? static_cast<const char *>(p.z) + act0 * kEl : nullptr;
+    const char *bb = static_cast<const char *>(p.Bm) + bc0 * kEl;
+    const char *cb = static_cast<const char *>(p.Cm) + bc0 * kEl;
+    char *yb = static_cast<char *>(p.y) + act0 * (OUT == 1 ? 2 : 4);
+    const uint32_t seg_n = (uint32_t)(t_end - t_begin);             // a multiple of 16
+    const uint32_t act_row = (uint32_t)((dcl - cg * kCh) * L);       // lane's channel row
+    // B/C staging: lane (j, q) moves timesteps 4j .. 4j+3 of state rows 2q and
+    // 2q+1 of B and C, i.e. the four entries bc[4j + i][q].
+    const int st_t = 4 * j;
+    const uint32_t bc_row = (uint32_t)(2 * q * L);
 
     struct Slot { Raw4<IN> u, dl, z, B0, B1, C0, C1; };
     Slot s0, s1;
     // Loads never branch: a chunk past the end of the segment reads the last
     // valid quad again (those values are never consumed), so the prefetch
     // registers are written in place every time.
-    auto issue_loads = [&](Slot &sl, int64_t t0) {
-        const int64_t ts = t0 + 4 * q < t_end - 4 ? t0 + 4 * q : t_end - 4;
-        sl.u.load(p.u, row * L + ts);
-        sl.dl.load(p.delta, row * L + ts);
-        if (GATE) sl.z.load(p.z, row * L + ts);
-        const int64_t tb = t0 + st_t < t_end - 4 ? t0 + st_t : t_end - 4;
-        sl.B0.load(p.Bm, st_row + tb);
-        sl.B1.load(p.Bm, st_row + L + tb);
-        sl.C0.load(p.Cm, st_row + tb);
-        sl.C1.load(p.Cm, st_row + L + tb);
+    auto issue_loads = [&](Slot &sl, uint32_t tr) {            // tr: chunk start within the segment
+        const uint32_t ta = tr + 4 * q < seg_n - 4 ? tr + 4 * q : seg_n - 4;
+        const uint32_t oa = act_row + ta;
+        sl.u.load(ub, oa);
+        sl.dl.load(db, oa);
+        if (GATE && !PREPASS) sl.z.load(zb, oa);
+        const uint32_t tb = tr + st_t < seg_n - 4 ? tr + st_t : seg_n - 4;
+        const uint32_t ob = bc_row + tb;
+        sl.B0.load(bb, ob);
+        sl.B1.load(bb, ob + (uint32_t)L);
+        if (!PREPASS) {
+            sl.C0.load(cb, ob);
+            sl.C1.load(cb, ob + (uint32_t)L);
+        }
     };
 
     // Phase B step TQ: timesteps 4 TQ .. 4 TQ + 3, operands already in registers.
+    float dsum_chunk = 0.0f;
     auto recur4 = [&](const f32x4 (&ddv)[2], const f32x4 (&bcv)[4], auto tq_c) {
         constexpr int TQ = decltype(tq_c)::value;
         float acc4[4];
@@ -145,14 +190,15 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
             const float a1 = hw_exp2(dl * a2[1]);
             h[0] = __builtin_fmaf(a0, h[0], dx * bcv[k][0]);
             h[1] = __builtin_fmaf(a1, h[1], dx * bcv[k][1]);
-            acc4[k] = __builtin_fmaf(bcv[k][3], h[1], bcv[k][2] * h[0]);
+            if (PREPASS) dsum_chunk += dl;
+            else acc4[k] = __builtin_fmaf(bcv[k][3], h[1], bcv[k][2] * h[0]);
         }
-        sm.part[TQ][j][q ^ TQ] = f32x4{acc4[0], acc4[1], acc4[2], acc4[3]};
+        if (!PREPASS) sm.part[kT / 4 * j + TQ][q] = f32x4{acc4[0], acc4[1], acc4[2], acc4[3]};
     };
     auto load4 = [&](f32x4 (&ddv)[2], f32x4 (&bcv)[4], auto tq_c) {
         constexpr int TQ = decltype(tq_c)::value;
 #pragma unroll
-        for (int k = 0; k < 2; ++k) ddv[k] = sm.dd[2 * TQ + k][j ^ ((2 * TQ + k) & 7)];
+        for (int k = 0; k < 2; ++k) ddv[k] = sm.dd[2 * TQ + k][j];
 #pragma unroll
         for (int k = 0; k < 4; ++k) bcv[k] = sm.bc[4 * TQ + k][q];
     };
@@ -177,18 +223,19 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
                 dl[k] = SOFTPLUS ? softplus_f32(v) : v;
                 dx[k] = dl[k] * x;
                 xs[k] = x;
-                if (GATE) gs[k] = silu_f32(sl.z.get(k));
+                if (GATE && !PREPASS) gs[k] = silu_f32(sl.z.get(k));
             }
-            sm.dd[2 * q][j ^ ((2 * q) & 7)] = f32x4{dl[0], dx[0], dl[1], dx[1]};
-            sm.dd[2 * q + 1][j ^ ((2 * q + 1) & 7)] = f32x4{dl[2], dx[2], dl[3], dx[3]};
+            sm.dd[2 * q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
+            sm.dd[2 * q + 1][j] = f32x4{dl[2], dx[2], dl[3], dx[3]};
         }
 #pragma unroll
         for (int k = 0; k < 4; ++k)
-            sm.bc[st_t + k][q] = f32x4{sl.B0.get(k), sl.B1.get(k), sl.C0.get(k), sl.C1.get(k)};
+            sm.bc[st_t + k][q] = PREPASS ? f32x4{sl.B0.get(k), sl.B1.get(k), 0.0f, 0.0f}
+                                         : f32x4{sl.B0.get(k), sl.B1.get(k), sl.C0.get(k), sl.C1.get(k)};
         wave_sync();
 
         // refill this slot with the chunk after next while the recurrence runs
-        issue_loads(sl, t0 + 2 * kT);
+        issue_loads(sl, (uint32_t)(t0 - t_begin) + 2 * kT);
 
         // ---- B: the recurrence, fully unrolled over the chunk; the operands of
         //      step i + 1 are read from LDS while step i computes ----------------
@@ -225,11 +272,17 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         }
         wave_sync();
 
+        if (PREPASS) {                              // two-level sum keeps the rounding small
+            dsum += dsum_chunk;
+            dsum_chunk = 0.0f;
+            return;
+        }
+
         // ---- C: sum the 8 partials of channel j at timesteps 4q .. 4q+3 --------
         if (4 * q < nt) {
-            f32x4 acc = sm.part[q][j][0 ^ q];
+            f32x4 acc = sm.part[kT / 4 * j + q][0];
 #pragma unroll
-            for (int w = 1; w < kQ; ++w) acc += sm.part[q][j][w ^ q];
+            for (int w = 1; w < kQ; ++w) acc += sm.part[kT / 4 * j + q][w];
             float yv[4];
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -238,21 +291,21 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
                 yv[k] = y;
             }
             if (live) {
-                const int64_t off = row * L + t0 + 4 * q;
+                const uint32_t oy = act_row + (uint32_t)(t0 - t_begin) + 4 * q;
                 if (OUT == 0) {
-                    *reinterpret_cast<f32x4 *>(static_cast<float *>(p.y) + off) = f32x4{yv[0], yv[1], yv[2], yv[3]};
+                    *reinterpret_cast<f32x4 *>(yb + oy * 4u) = f32x4{yv[0], yv[1], yv[2], yv[3]};
                 } else {
                     const uint32_t w0 = (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
                     const uint32_t w1 = (uint32_t)f32_to_bf16(yv[2]) | ((uint32_t)f32_to_bf16(yv[3]) << 16);
-                    *reinterpret_cast<u32x2 *>(static_cast<uint16_t *>(p.y) + off) = u32x2{w0, w1};
+                    *reinterpret_cast<u32x2 *>(yb + oy * 2u) = u32x2{w0, w1};
                 }
             }
         }
         wave_sync();   // part / dd / bc are rewritten by the next chunk
     };
 
-    issue_loads(s0, t_begin);
-    issue_loads(s1, t_begin + kT);
+    issue_loads(s0, 0);
+    issue_loads(s1, kT);
     int64_t t0 = t_begin;
     for (; t0 + 2 * kT <= t_end; t0 += 2 * kT) {   // pairs of full chunks
         chunk(s0, t0);
@@ -261,7 +314,12 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     if (t0 < t_end) chunk(s0, t0);                  // a full chunk and/or a half chunk remain
     if (t0 + kT < t_end) chunk(s1, t0 + kT);
 
-    if (p.h_last && live) {
+    if (PREPASS) {
+        if (live) {
+            const float P0 = hw_exp2(a2[0] * dsum), P1 = hw_exp2(a2[1] * dsum);
+            *reinterpret_cast<f32x4 *>(carry + ((seg * rows + row) * kN + n0) * 2) = f32x4{P0, h[0], P1, h[1]};
+        }
+    } else if (p.h_last && live && seg == nseg - 1) {
 #pragma unroll
         for (int s = 0; s < 2; ++s) p.h_last[row * kN + n0 + s] = h[s];
     }

@@ -27,15 +27,19 @@ def test_tiny_config_full():
     run_case(inp)
 
 
+# Lengths that are multiples of 16 take the tiled kernel (1008 ends in a half
+# chunk); other lengths take the row-per-thread kernel.  dim 200 leaves dead
+# lanes in the last 8-channel group.
+@pytest.mark.parametrize("L", [1008, 1000])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("gated,with_h0", [(True, True), (False, False), (True, False)])
-def test_ragged_multi_tile(dtype, gated, with_h0):
-    inp = make_inputs(2, 200, 1000, 16, dtype=dtype, seed=1, gated=gated, with_h0=with_h0)
-    announce(f"ragged (2, 200, 1000) {dtype} gated={gated} h0={with_h0}")
+def test_ragged_multi_tile(dtype, gated, with_h0, L):
+    inp = make_inputs(2, 200, L, 16, dtype=dtype, seed=1, gated=gated, with_h0=with_h0)
+    announce(f"ragged (2, 200, {L}) {dtype} gated={gated} h0={with_h0}")
     run_case(inp)
 
 
-@pytest.mark.parametrize("L", [1, 2, 3, 63, 64, 65, 127, 511, 513, 4097])
+@pytest.mark.parametrize("L", [1, 2, 3, 16, 32, 48, 63, 64, 65, 80, 127, 511, 513, 4096, 4097, 4112])
 def test_edge_lengths(L):
     inp = make_inputs(3, 130, L, 16, dtype="bf16", seed=2, with_h0=True)
     announce(f"edge length L={L} (3, 130) bf16")
@@ -49,23 +53,23 @@ def test_dskip_zero_isolates_ssm_term():
 
 
 def test_random_A():
-    inp = make_inputs(2, 160, 1500, 16, dtype="bf16", seed=4, with_h0=True, A_kind="random")
-    announce("random A (2, 160, 1500)")
+    inp = make_inputs(2, 160, 1504, 16, dtype="bf16", seed=4, with_h0=True, A_kind="random")
+    announce("random A (2, 160, 1504)")
     run_case(inp)
 
 
 def test_extreme_delta():
-    inp = make_inputs(1, 128, 700, 16, dtype="f32", seed=5, with_h0=True)
+    inp = make_inputs(1, 128, 704, 16, dtype="f32", seed=5, with_h0=True)
     rng = np.random.default_rng(55)
     inp.delta = (8.0 * rng.standard_normal(inp.delta.shape)).astype(np.float32)   # +-8 sigma
-    announce("extreme delta_raw (1, 128, 700)")
+    announce("extreme delta_raw (1, 128, 704)")
     run_case(inp)
 
 
 def test_large_h0():
-    inp = make_inputs(2, 64, 300, 16, dtype="bf16", seed=6, with_h0=True)
+    inp = make_inputs(2, 64, 304, 16, dtype="bf16", seed=6, with_h0=True)
     inp.h0 = (inp.h0 * 100.0).astype(np.float32)
-    announce("h0 x 100 (2, 64, 300)")
+    announce("h0 x 100 (2, 64, 304)")
     run_case(inp)
 
 
@@ -85,8 +89,8 @@ def test_small_dstate(N):
 
 
 def test_bf16_output():
-    inp = make_inputs(2, 128, 900, 16, dtype="bf16", seed=9)
-    announce("bf16 output (2, 128, 900)")
+    inp = make_inputs(2, 128, 912, 16, dtype="bf16", seed=9)
+    announce("bf16 output (2, 128, 912)")
     y, h = gpu_fwd(inp, out_dtype=torch.bfloat16)
     assert y.dtype == torch.bfloat16
     check_against_oracle(inp, y, h, tol_y=BF16_OUT_TOL)
@@ -102,10 +106,11 @@ def test_seqlen_zero_returns_h0():
     assert np.all(h.cpu().numpy() == 0)
 
 
-def test_h_last_may_alias_h0():
+@pytest.mark.parametrize("L", [256, 257])
+def test_h_last_may_alias_h0(L):
     import paper_2401_13660_amd as mb
-    inp = make_inputs(2, 100, 257, 16, dtype="bf16", seed=11, with_h0=True)
-    announce("h_last is h0 (2, 100, 257)")
+    inp = make_inputs(2, 100, L, 16, dtype="bf16", seed=11, with_h0=True)
+    announce(f"h_last is h0 (2, 100, {L})")
     t = to_device(inp)
     state = t["h0"].clone()
     y, h = mb.scan_fwd(t["u"], t["delta"], t["A"], t["B"], t["C"], D=t["Dskip"], dt_bias=t["dt_bias"],
@@ -119,9 +124,9 @@ def test_resume_split_on_gpu():
     """Scanning two halves with the carried state equals scanning the whole (Alg. 1 resume)."""
     import paper_2401_13660_amd as mb
     inp = make_inputs(2, 96, 1200, 16, dtype="bf16", seed=12, with_h0=True)
-    announce("split resume (2, 96, 1200) at k=517")
+    announce("split resume (2, 96, 1200) at k=512")
     t = to_device(inp)
-    k = 517
+    k = 512
     common = dict(D=t["Dskip"], dt_bias=t["dt_bias"])
     sl = lambda x, a, b: x[..., a:b].contiguous()
     y1, h1 = mb.scan_fwd(sl(t["u"], 0, k), sl(t["delta"], 0, k), t["A"], sl(t["B"], 0, k), sl(t["C"], 0, k),
@@ -133,8 +138,27 @@ def test_resume_split_on_gpu():
 
 
 def test_deterministic():
-    inp = make_inputs(2, 256, 3000, 16, dtype="bf16", seed=13, with_h0=True)
-    announce("determinism (2, 256, 3000)")
+    inp = make_inputs(2, 256, 3008, 16, dtype="bf16", seed=13, with_h0=True)
+    announce("determinism (2, 256, 3008)")
+    y1, h1 = gpu_fwd(inp)
+    y2, h2 = gpu_fwd(inp)
+    assert torch.equal(y1, y2) and torch.equal(h1, h2)
+
+
+@pytest.mark.parametrize("shape", [(1, 64, 4096), (1, 61, 4112), (2, 24, 8192), (1, 8, 640)])
+@pytest.mark.parametrize("gated", [True, False])
+def test_time_segments(shape, gated):
+    """Few (batch, channel) rows and a long sequence: the tiled path cuts time into
+    segments, a pre-pass computes each segment's aggregate and the scan folds them."""
+    nb, dim, L = shape
+    inp = make_inputs(nb, dim, L, 16, dtype="bf16", seed=15, with_h0=True, gated=gated, A_kind="random")
+    announce(f"time segments {shape} gated={gated}")
+    run_case(inp)
+
+
+def test_time_segments_deterministic():
+    inp = make_inputs(1, 64, 4096, 16, dtype="bf16", seed=16, with_h0=True)
+    announce("time segments determinism (1, 64, 4096)")
     y1, h1 = gpu_fwd(inp)
     y2, h2 = gpu_fwd(inp)
     assert torch.equal(y1, y2) and torch.equal(h1, h2)
