@@ -26,6 +26,14 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
+
+# ALU roofline of the scan (derivation in the design doc section 7.1): per element the
+# method needs 16 exponentials and 64 other fp32 VALU operations for the 16-state
+# recurrence, plus at least 4 transcendentals and 12 VALU operations of
+# per-element work.  MI355X: 1024 SIMDs at 2.4 GHz; a wave64 fp32 VALU op every
+# 2 cycles (157.3 TFLOP/s), a transcendental every 8 (quarter rate).
+ALU_SIMD_CYCLES_PER_ELEMENT = (20 * 8 + 76 * 2) / 64.0
+ALU_PEAK_GELEMS = 1024 * 2.4e9 / ALU_SIMD_CYCLES_PER_ELEMENT / 1e9
 METRIC = "selective-scan GB/s & %HBM peak (972M layer, L=8192); B·L·D elems/s"
 DEFAULT_WORKLOAD = "mambabyte972m_L8192"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
@@ -43,6 +51,19 @@ def algorithmic_bytes(inp, out_bytes=4, want_h_last=False) -> int:
     state = inp.batch * inp.dim * inp.dstate * 4
     b += state * ((inp.h0 is not None) + bool(want_h_last))
     return int(b)
+
+
+def step_bytes(inp) -> int:
+    """Algorithmic bytes of seqlen successive one-byte steps: each step reads its
+    activations, B_t, C_t and the parameters, reads and writes the whole state,
+    and writes y_t."""
+    act = 2 if inp.dtype == "bf16" else 4
+    rows = inp.batch * inp.dim
+    per = rows * ((2 + (inp.z is not None)) * act + 4)
+    per += 2 * inp.batch * inp.dstate * act
+    per += inp.dim * inp.dstate * 4 + inp.dim * 4 * ((inp.Dskip is not None) + (inp.dt_bias is not None))
+    per += 2 * rows * inp.dstate * 4
+    return int(per * inp.seqlen)
 
 
 def kernel_sources_digest() -> str:
@@ -96,6 +117,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mode", choices=["fwd", "step"], default="fwd",
+                    help="fwd: one mb_scan_fwd per step; step: seqlen successive mb_scan_step calls per step "
+                         "(the recurrent-generation form of the same workload)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the scan, run a plain device copy of MIB MiB (reference for HBM counters)")
     args = ap.parse_args()
@@ -135,9 +159,22 @@ def main():
     y = torch.empty((inp.batch, inp.dim, inp.seqlen), dtype=torch.float32, device=dev)
     h_last = torch.empty((inp.batch, inp.dim, inp.dstate), dtype=torch.float32, device=dev) if want_h_last else None
 
-    def step():
-        mb.scan_fwd(g["u"], g["delta"], g["A"], g["B"], g["C"], D=g.get("Dskip"), dt_bias=g.get("dt_bias"),
-                    z=g.get("z"), h0=g.get("h0"), out=y, h_last=h_last)
+    if args.mode == "fwd":
+        def step():
+            mb.scan_fwd(g["u"], g["delta"], g["A"], g["B"], g["C"], D=g.get("Dskip"), dt_bias=g.get("dt_bias"),
+                        z=g.get("z"), h0=g.get("h0"), out=y, h_last=h_last)
+    else:
+        # per-byte slices made once, outside the timed region
+        cols = [{k: (v[..., i].contiguous() if k in ("u", "delta", "z", "B", "C") else None)
+                 for k, v in g.items()} for i in range(inp.seqlen)]
+        state = g["h0"].clone() if g.get("h0") is not None else torch.zeros(
+            (inp.batch, inp.dim, inp.dstate), dtype=torch.float32, device=dev)
+        ycols = [torch.empty((inp.batch, inp.dim), dtype=torch.float32, device=dev) for _ in range(inp.seqlen)]
+
+        def step():
+            for i, c in enumerate(cols):
+                mb.scan_step(state, c["u"], c["delta"], g["A"], c["B"], c["C"], D=g.get("Dskip"),
+                             dt_bias=g.get("dt_bias"), z_t=c.get("z"), out=ycols[i])
 
     for _ in range(args.warmup):
         step()
@@ -152,6 +189,8 @@ def main():
 
     E = inp.batch * inp.dim * inp.seqlen
     nbytes = algorithmic_bytes(inp, 4, want_h_last)
+    if args.mode == "step":
+        nbytes = step_bytes(inp)
     gbs = nbytes / (ms * 1e-3) / 1e9
     traffic = measured_traffic(args.workload)
 
@@ -160,16 +199,24 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": args.workload, **{k: v for k, v in WORKLOADS[args.workload].items()},
+        "config": {"workload": args.workload, "mode": args.mode,
+                   **{k: v for k, v in WORKLOADS[args.workload].items()},
                    "gated": inp.z is not None, "h0": inp.h0 is not None, "h_last": want_h_last,
                    "out_dtype": "f32", "parallelism": "single GPU"},
         "elems_per_s": round(E / (ms * 1e-3), 1),
         "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
-        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "algorithmic_bytes": nbytes},
+        "roofline": {"bound": "alu", "achieved": round(E / (ms * 1e-3) / 1e9, 2),
+                     "peak": round(ALU_PEAK_GELEMS, 1), "unit": "Gelem/s",
+                     "frac": round(E / (ms * 1e-3) / 1e9 / ALU_PEAK_GELEMS, 4), "traffic": traffic,
+                     "hbm": {"achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": round(gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": nbytes}},
     }
-    if not args.no_cpu_baseline:
+    if args.mode == "step":
+        # one-byte steps are bound by moving the state: report against HBM
+        line["roofline"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                            "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                            "note": "includes host launch gaps between the per-byte calls"}
+    if not args.no_cpu_baseline and args.mode == "fwd":
         cb = cpu_baseline(inp, y)
         line["cpu_baseline"] = {
             "value": round(cb["elems_per_s"] * nbytes / E / 1e9, 3), "unit": "GB/s",

@@ -31,20 +31,18 @@ __device__ __forceinline__ float hw_exp2(float x) { return __builtin_amdgcn_exp2
 __device__ __forceinline__ float hw_log2(float x) { return __builtin_amdgcn_logf(x); }
 __device__ __forceinline__ float hw_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
-// softplus(v) = log(1 + e^v), the positivity map of the timestep (eq. (3)).
-// For v > 20 the correction log1p(e^-v) < 2.1e-9 is below half an ulp of v.
-// Otherwise log1p(e) with e = e^v is taken as log(w) with w = fl(1 + e), plus
-// the first-order term c / w of the rounding error c = e - (w - 1) (exact in
-// fp32).  The term only matters for small e, where w is close to 1 and
-// (2 - w) is an accurate stand-in for 1 / w; for w >= 2 it is below 2^-24 of
-// log(w) and is dropped (the clamp keeps (2 - w) from amplifying c).
+// softplus(v) = log(1 + e^v), the positivity map of the timestep (eq. (3)),
+// as max(v, 0) + log1p(e) with e = e^-|v| in (0, 1].  log1p(e) is taken as
+// log(w) with w = fl(1 + e) in [1, 2], plus the rounding error c = e - (w - 1)
+// (exact in fp32 by Sterbenz) divided by w; using c for c / w leaves an error
+// of at most c * e <= 2^-24 * e, i.e. relative 2^-24, so the result is
+// accurate to a few ulp for every v, including large negative v where the
+// naive log(1 + e^v) loses all digits.
 __device__ __forceinline__ float softplus_f32(float v) {
-    const float e = hw_exp2(v * kLog2e);
+    const float e = hw_exp2(-__builtin_fabsf(v) * kLog2e);
     const float w = 1.0f + e;
     const float c = e - (w - 1.0f);
-    const float lg = hw_log2(w) * kLn2;
-    const float sp = __builtin_fmaf(c, __builtin_fmaxf(2.0f - w, 0.0f), lg);
-    return v > 20.0f ? v : sp;
+    return __builtin_fmaxf(v, 0.0f) + __builtin_fmaf(hw_log2(w), kLn2, c);
 }
 
 // silu(z) = z * sigmoid(z), the Swish gate (Table 8, Fig. 5).
