@@ -58,6 +58,11 @@ class Oracle:
         self.lib.mbo_scan_rows.argtypes = [
             ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
             _D, _D, _D, _D, _D, _D, _D, _I64, ctypes.c_int64, _D, _D, _D, _D]
+        self.lib.mbo_scan_rows_states.restype = ctypes.c_int
+        self.lib.mbo_scan_rows_states.argtypes = [
+            ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+            _D, _D, _D, _D, _D, _D, _D, _I64, ctypes.c_int64, _D, _D, _D, _D,
+            _I64, ctypes.c_int64, _D]
         self.lib.mbo_max_threads.restype = ctypes.c_int
         self.lib.mbo_scan_step.restype = ctypes.c_int
         self.lib.mbo_scan_step.argtypes = [
@@ -69,12 +74,14 @@ class Oracle:
 
     # -- rows ---------------------------------------------------------------
     def scan_rows(self, u, delta, A, Bm, Cm, bidx, *, z=None, Dskip=None, dt_bias=None,
-                  h0=None, delta_softplus=True, want_h_last=True):
+                  h0=None, delta_softplus=True, want_h_last=True, positions=None):
         """Scan R independent rows.
 
         u, delta, z: (R, L); A, h0: (R, N); Dskip, dt_bias: (R,);
         Bm, Cm: (nbatch, N, L); bidx: (R,) batch index of each row.
-        All float arguments must already be fp64.  Returns (y (R, L), h_last (R, N) or None).
+        All float arguments must already be fp64.  Returns (y (R, L), h_last (R, N) or None),
+        and with ``positions`` (R, P) integers also h_pos (R, P, N): the state after
+        each requested timestep (-1: the initial state; outside [-1, L-1]: NaN).
         """
         u = np.ascontiguousarray(u, dtype=np.float64)
         R, L = u.shape
@@ -88,23 +95,38 @@ class Oracle:
         bidx = np.ascontiguousarray(bidx, dtype=np.int64)
         y = np.empty((R, L), dtype=np.float64)
         h_last = np.empty((R, N), dtype=np.float64) if want_h_last else None
-        rc = self.lib.mbo_scan_rows(R, L, N, int(bool(delta_softplus)),
-                                    _ptr(u), _ptr(a["delta"]), _ptr(a["z"]), _ptr(a["A"]),
-                                    _ptr(a["Dskip"]), _ptr(a["dt_bias"]), _ptr(a["h0"]),
-                                    bidx.ctypes.data_as(_I64), nb, _ptr(Bm), _ptr(a["Cm"]),
-                                    _ptr(y), _ptr(h_last))
+        if positions is None:
+            rc = self.lib.mbo_scan_rows(R, L, N, int(bool(delta_softplus)),
+                                        _ptr(u), _ptr(a["delta"]), _ptr(a["z"]), _ptr(a["A"]),
+                                        _ptr(a["Dskip"]), _ptr(a["dt_bias"]), _ptr(a["h0"]),
+                                        bidx.ctypes.data_as(_I64), nb, _ptr(Bm), _ptr(a["Cm"]),
+                                        _ptr(y), _ptr(h_last))
+            if rc != 0:
+                raise ValueError(f"oracle rejected the arguments (status {rc})")
+            return y, h_last
+        pos = np.ascontiguousarray(positions, dtype=np.int64).reshape(R, -1)
+        P = pos.shape[1]
+        h_pos = np.empty((R, P, N), dtype=np.float64)
+        rc = self.lib.mbo_scan_rows_states(R, L, N, int(bool(delta_softplus)),
+                                           _ptr(u), _ptr(a["delta"]), _ptr(a["z"]), _ptr(a["A"]),
+                                           _ptr(a["Dskip"]), _ptr(a["dt_bias"]), _ptr(a["h0"]),
+                                           bidx.ctypes.data_as(_I64), nb, _ptr(Bm), _ptr(a["Cm"]),
+                                           _ptr(y), _ptr(h_last), pos.ctypes.data_as(_I64), P,
+                                           _ptr(h_pos))
         if rc != 0:
             raise ValueError(f"oracle rejected the arguments (status {rc})")
-        return y, h_last
+        return y, h_last, h_pos
 
     # -- whole tensors --------------------------------------------------------
     def scan_fwd(self, u, delta, A, Bm, Cm, *, z=None, Dskip=None, dt_bias=None, h0=None,
-                 delta_softplus=True, dtype: str | None = None, rows=None):
+                 delta_softplus=True, dtype: str | None = None, rows=None, positions=None):
         """Scan (batch, dim, L) tensors; ``rows`` optionally picks flat (b*dim + d) rows.
 
         Activations may be bf16 bit patterns (``dtype="bf16"``) or floats.
         Returns y of shape (batch, dim, L) -- or (len(rows), L) -- and h_last
-        of shape (batch, dim, N) -- or (len(rows), N) -- in fp64.
+        of shape (batch, dim, N) -- or (len(rows), N) -- in fp64.  With
+        ``positions`` of shape (npos, batch) (position k of batch element b) it
+        also returns the states there, (npos, batch, dim, N) -- or (npos, len(rows), N).
         """
         u = np.asarray(u)
         nb, dim, L = u.shape
@@ -117,16 +139,26 @@ class Oracle:
             return None if x is None else to_f64(np.asarray(x).reshape(nb * dim, -1)[flat], dtype)
 
         Af = to_f64(A)[didx]
-        y, h_last = self.scan_rows(
+        row_pos = None
+        if positions is not None:
+            pos = np.asarray(positions, dtype=np.int64).reshape(-1, nb)
+            row_pos = np.ascontiguousarray(pos[:, bidx].T)                 # (rows, npos)
+        out = self.scan_rows(
             act(u), act(delta), Af, to_f64(Bm, dtype), to_f64(Cm, dtype), bidx,
             z=act(z),
             Dskip=None if Dskip is None else to_f64(Dskip)[didx],
             dt_bias=None if dt_bias is None else to_f64(dt_bias)[didx],
             h0=None if h0 is None else to_f64(h0).reshape(nb * dim, N)[flat],
-            delta_softplus=delta_softplus)
+            delta_softplus=delta_softplus, positions=row_pos)
+        y, h_last = out[0], out[1]
         if rows is None:
-            return y.reshape(nb, dim, L), h_last.reshape(nb, dim, N)
-        return y, h_last
+            y, h_last = y.reshape(nb, dim, L), h_last.reshape(nb, dim, N)
+        if positions is None:
+            return y, h_last
+        h_pos = np.moveaxis(out[2], 1, 0)                                  # (npos, rows, N)
+        if rows is None:
+            h_pos = h_pos.reshape(-1, nb, dim, N)
+        return y, h_last, h_pos
 
     def scan_step(self, h, u_t, delta_t, A, B_t, C_t, *, z_t=None, Dskip=None, dt_bias=None,
                   delta_softplus=True, dtype: str | None = None):
@@ -166,8 +198,8 @@ def default() -> Oracle:
     return _default
 
 
-def scan_inputs(inp, rows=None, delta_softplus=True):
+def scan_inputs(inp, rows=None, delta_softplus=True, positions=None):
     """Run the oracle on a ``ScanInputs`` workload (any object with the same fields)."""
     return default().scan_fwd(inp.u, inp.delta, inp.A, inp.B, inp.C, z=inp.z, Dskip=inp.Dskip,
                               dt_bias=inp.dt_bias, h0=inp.h0, delta_softplus=delta_softplus,
-                              dtype=inp.dtype, rows=rows)
+                              dtype=inp.dtype, rows=rows, positions=positions)

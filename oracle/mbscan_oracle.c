@@ -22,7 +22,12 @@
  *   yv     = sum_n C[b][n][t] * h[n] + Dskip[r] * u[r][t]   (eq. (2) y = C h, plus the skip term of Table 8)
  *   y[r][t]= yv * silu(z[r][t]) if z is given, else yv      (Table 8 "Element-wise gating"; Fig. 5 Swish gate)
  *
- * and h_last[r] = h after the final step.  b = bidx[r] selects the batch
+ * and h_last[r] = h after the final step.  Optionally the state is also
+ * recorded at requested positions: h_pos[r][k] = h after timestep pos[r][k],
+ * where position -1 is the initial state and a position outside [-1, L-1]
+ * reads NaN (the verifier of Appendix F, Algorithm 1, resumes from the state
+ * at the bifurcation position c; Section 3, speculative decoding paragraph).
+ * b = bidx[r] selects the batch
  * element whose B and C rows (shape N x L, time contiguous) the row reads:
  * B and C are shared by all channels of a batch element (Section 2, after
  * eq. (3)); A, Dskip and dt_bias are per channel.
@@ -33,7 +38,8 @@
  * Parity pinned by tests/test_oracle_pins.py (brute-force materialisation on
  * the time grid t_k = sum Delta, geometric closed form, B = 0, split
  * invariance, the eq. (4) gated-recurrence special case, the associative
- * tuple scan, N-separability, linearity, step == forward, the Delta limits).
+ * tuple scan, N-separability, linearity, step == forward, the Delta limits,
+ * states at positions against the time-grid closed form of every state).
  */
 #include <math.h>
 #include <stddef.h>
@@ -61,17 +67,38 @@ static double silu(double z)
     return z / (1.0 + exp(-z));
 }
 
+/* Copy the state after timestep t (t = -1: before the first step) into every
+ * slot k whose requested position is t; when t = -1 also mark the slots whose
+ * position lies outside [-1, L-1] with NaN. */
+static void record_states(int64_t t, int64_t L, int64_t N, const double *h,
+                          const int64_t *pos, int64_t P, double *out)
+{
+    for (int64_t k = 0; k < P; ++k) {
+        if (pos[k] == t) {
+            for (int64_t n = 0; n < N; ++n)
+                out[k * N + n] = h[n];
+        } else if (t == -1 && (pos[k] < -1 || pos[k] >= L)) {
+            for (int64_t n = 0; n < N; ++n)
+                out[k * N + n] = NAN;
+        }
+    }
+}
+
 static void scan_one_row(int64_t r, int64_t L, int64_t N, int delta_softplus,
                          const double *u, const double *delta, const double *z,
                          const double *A, const double *Dskip, const double *dt_bias,
                          const double *h0, const int64_t *bidx,
                          const double *Bm, const double *Cm,
-                         double *y, double *h_last)
+                         double *y, double *h_last,
+                         const int64_t *pos, int64_t P, double *h_pos)
 {
     double h[MBO_MAX_N];
     const int64_t b = bidx[r];
     for (int64_t n = 0; n < N; ++n)
         h[n] = h0 ? h0[r * N + n] : 0.0;
+    const int64_t *row_pos = P > 0 ? pos + r * P : NULL;
+    double *row_out = P > 0 ? h_pos + r * P * N : NULL;
+    record_states(-1, L, N, h, row_pos, P, row_out);
 
     for (int64_t t = 0; t < L; ++t) {
         const double x = u[r * L + t];
@@ -86,6 +113,7 @@ static void scan_one_row(int64_t r, int64_t L, int64_t N, int delta_softplus,
         }
         const double yv = acc + (Dskip ? Dskip[r] * x : 0.0);
         y[r * L + t] = z ? yv * silu(z[r * L + t]) : yv;
+        record_states(t, L, N, h, row_pos, P, row_out);
     }
     if (h_last)
         for (int64_t n = 0; n < N; ++n)
@@ -103,20 +131,25 @@ static void scan_one_row(int64_t r, int64_t L, int64_t N, int delta_softplus,
  *   Bm, Cm      : nbatch x N x L
  *   y           : R x L     (output)
  *   h_last      : R x N     (output, may be NULL)
+ *   pos         : R x P     (requested positions of each row, may be NULL when P = 0)
+ *   h_pos       : R x P x N (output: the state at each requested position)
  * Returns 0, or -1 on a bad argument (nothing written).
  */
-int mbo_scan_rows(int64_t R, int64_t L, int64_t N, int delta_softplus,
-                  const double *u, const double *delta, const double *z,
-                  const double *A, const double *Dskip, const double *dt_bias,
-                  const double *h0, const int64_t *bidx, int64_t nbatch,
-                  const double *Bm, const double *Cm,
-                  double *y, double *h_last)
+int mbo_scan_rows_states(int64_t R, int64_t L, int64_t N, int delta_softplus,
+                         const double *u, const double *delta, const double *z,
+                         const double *A, const double *Dskip, const double *dt_bias,
+                         const double *h0, const int64_t *bidx, int64_t nbatch,
+                         const double *Bm, const double *Cm,
+                         double *y, double *h_last,
+                         const int64_t *pos, int64_t P, double *h_pos)
 {
-    if (R < 0 || L < 0 || N < 1 || N > MBO_MAX_N || nbatch < 1)
+    if (R < 0 || L < 0 || N < 1 || N > MBO_MAX_N || nbatch < 1 || P < 0)
         return MBO_ERR_ARG;
     if (R == 0)
         return MBO_OK;
     if (!u || !delta || !A || !bidx || !Bm || !Cm || (!y && L > 0))
+        return MBO_ERR_ARG;
+    if (P > 0 && (!pos || !h_pos))
         return MBO_ERR_ARG;
     for (int64_t r = 0; r < R; ++r)
         if (bidx[r] < 0 || bidx[r] >= nbatch)
@@ -125,8 +158,20 @@ int mbo_scan_rows(int64_t R, int64_t L, int64_t N, int delta_softplus,
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t r = 0; r < R; ++r)
         scan_one_row(r, L, N, delta_softplus, u, delta, z, A, Dskip, dt_bias,
-                     h0, bidx, Bm, Cm, y, h_last);
+                     h0, bidx, Bm, Cm, y, h_last, pos, P, h_pos);
     return MBO_OK;
+}
+
+/* The forward scan without recorded positions. */
+int mbo_scan_rows(int64_t R, int64_t L, int64_t N, int delta_softplus,
+                  const double *u, const double *delta, const double *z,
+                  const double *A, const double *Dskip, const double *dt_bias,
+                  const double *h0, const int64_t *bidx, int64_t nbatch,
+                  const double *Bm, const double *Cm,
+                  double *y, double *h_last)
+{
+    return mbo_scan_rows_states(R, L, N, delta_softplus, u, delta, z, A, Dskip, dt_bias,
+                                h0, bidx, nbatch, Bm, Cm, y, h_last, NULL, 0, NULL);
 }
 
 /*
@@ -160,7 +205,7 @@ int mbo_scan_step(int64_t R, int64_t N, int delta_softplus,
     for (int64_t r = 0; r < R; ++r) {
         /* B_t and C_t are (nbatch, N): the L = 1 case of the (nbatch, N, L) layout. */
         scan_one_row(r, 1, N, delta_softplus, u_t, delta_t, z_t, A, Dskip, dt_bias,
-                     h, bidx, B_t, C_t, y_t, h);
+                     h, bidx, B_t, C_t, y_t, h, NULL, 0, NULL);
     }
     return MBO_OK;
 }

@@ -59,13 +59,15 @@ def _run(orc, c, **kw):
                         dt_bias=c["dt_bias"], h0=c["h0"], **kw)
 
 
-def _brute(c, delta_softplus=True):
-    """Time-grid closed form of every state (eq. (1) solved on t_k = sum Delta)."""
+def _brute(c, delta_softplus=True, all_states=False):
+    """Time-grid closed form of every state (eq. (1) solved on t_k = sum Delta).
+    With ``all_states`` also returns h_t for every t, shape (nb, dim, L, N)."""
     u, A, Bm, Cm = c["u"], c["A"], c["B"], c["C"]
     nb, dim, L = u.shape
     N = A.shape[1]
     y = np.zeros((nb, dim, L))
     h_last = np.zeros((nb, dim, N))
+    h_all = np.zeros((nb, dim, L, N))
     for b in range(nb):
         for d in range(dim):
             v = c["delta"][b, d] + (0.0 if c["dt_bias"] is None else c["dt_bias"][d])
@@ -76,13 +78,14 @@ def _brute(c, delta_softplus=True):
                 w = np.exp(np.outer(A[d], S[t] - S[: t + 1]))          # (N, t+1) decay from s to t
                 inp = dl[: t + 1] * Bm[b, :, : t + 1] * u[b, d, : t + 1]  # Euler B-bar x at each s
                 h = np.exp(A[d] * S[t]) * h0 + (w * inp).sum(axis=1)
+                h_all[b, d, t] = h
                 yv = Cm[b, :, t] @ h + (0.0 if c["Dskip"] is None else c["Dskip"][d]) * u[b, d, t]
                 if c["z"] is not None:
                     zz = c["z"][b, d, t]
                     yv = yv * zz * expit(zz)
                 y[b, d, t] = yv
             h_last[b, d] = h if L > 0 else h0
-    return y, h_last
+    return (y, h_last, h_all) if all_states else (y, h_last)
 
 
 # ---------------------------------------------------------------------------
@@ -303,8 +306,36 @@ def pin_softplus_extremes(orc):
     assert rel <= 1e-14, f"softplus elementwise relative error {rel:.3e}"
 
 
+def pin_states_at_positions(orc):
+    """Appendix F, Algorithm 1 restarts from h_c: the state recorded at position p is
+    the time-grid closed form of h_p, p = -1 is the initial state, and a position
+    outside [-1, L-1] reads NaN; recording changes neither y nor h_last."""
+    for seed, kw in ((7, {}), (8, dict(h0=False, gated=False))):
+        c = _rand_case(seed, nb=3, dim=2, L=24, N=3, **kw)
+        L = c["u"].shape[2]
+        pos = np.array([[-1, 5, L + 6],        # position k = 0 of batch elements 0, 1, 2
+                        [0, 5, -2],            # k = 1 (a repeat, an invalid position)
+                        [L - 1, 11, L - 1]])   # k = 2
+        y, h, hp = _run(orc, c, positions=pos)
+        y0, h0_ = _run(orc, c)
+        assert np.array_equal(y, y0) and np.array_equal(h, h0_), "positions changed y or h_last"
+        ry, rh, rall = _brute(c, all_states=True)
+        init = np.zeros_like(rh) if c["h0"] is None else c["h0"]
+        for k in range(pos.shape[0]):
+            for b in range(pos.shape[1]):
+                p = pos[k, b]
+                if p == -1:
+                    ref = init[b]
+                elif 0 <= p < L:
+                    ref = rall[b, :, p]
+                else:
+                    assert np.all(np.isnan(hp[k, b])), f"invalid position {p} not NaN"
+                    continue
+                _close(hp[k, b], ref, 1e-11, f"state at position {p} (seed {seed}, k {k}, b {b})")
+
+
 ALL_PINS = [
     pin_golden_decimal, pin_bruteforce, pin_geometric, pin_B_zero, pin_split, pin_eq4,
     pin_tuple_scan, pin_separability, pin_linearity, pin_step_equals_fwd, pin_limits,
-    pin_softplus_extremes,
+    pin_softplus_extremes, pin_states_at_positions,
 ]

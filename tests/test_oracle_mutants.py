@@ -46,6 +46,10 @@ MUTANTS = [
     ("h_last_stale", "h_last[r * N + n] = h[n];", "h_last[r * N + n] = h0 ? h0[r * N + n] : 0.0;"),
     ("delta_from_prev_t", "double v = delta[r * L + t]", "double v = delta[r * L + (t > 0 ? t - 1 : 0)]"),
     ("C_state_shift", "acc += Cm[(b * N + n) * L + t] * h[n];", "acc += Cm[(b * N + (n + 1) % N) * L + t] * h[n];"),
+    ("position_off_by_one", "record_states(t, L, N, h, row_pos, P, row_out);",
+     "record_states(t + 1, L, N, h, row_pos, P, row_out);"),
+    ("position_initial_dropped", "record_states(-1, L, N, h, row_pos, P, row_out);", ""),
+    ("position_invalid_zero", "out[k * N + n] = NAN;", "out[k * N + n] = 0.0;"),
     ("last_state_dropped_from_y", "for (int64_t n = 0; n < N; ++n) {\n            const double abar",
      "for (int64_t n = 0; n < N; ++n) {\n            if (n == N - 1 && N > 1) continue;\n            const double abar"),
 ]
