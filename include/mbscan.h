@@ -13,7 +13,7 @@
  * state h0 and optionally returning the final state: the resume capability
  * that speculative decoding needs to verify a drafted byte chunk from the
  * cached state and continue from it (Section 3 "Speculative decoding through
- * subword drafting"; Appendix G, Algorithm 1).  mb_scan_step is the
+ * subword drafting"; Appendix F, Algorithm 1).  mb_scan_step is the
  * one-byte recurrent update used during generation (Section 2: the recurrence
  * is run directly at inference).
  *
@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define MB_ABI_VERSION 1
+#define MB_ABI_VERSION 2
 
 typedef enum {
     MB_F32 = 0,
@@ -102,6 +102,41 @@ int mb_scan_fwd(const mb_scan_desc *desc,
                 const void *Bmat, const void *Cmat,
                 const float *Dskip, const float *dt_bias, const void *z,
                 const float *h0, void *y, float *h_last, void *stream);
+
+/*
+ * mb_scan_fwd that also records the state at requested positions.  The
+ * verifier of Algorithm 1 (Appendix F) scans the drafted bytes in parallel,
+ * finds the bifurcation position c and continues byte by byte from h_c; the
+ * resumable scan of Section 3 ("Speculative decoding through subword
+ * drafting") restarts from that state instead of from the first byte.
+ *
+ *   pos    int32 (npos, B)        pos[k * B + b] is the k-th requested
+ *                                 position of batch element b: a timestep
+ *                                 0 <= p < L, or -1 for the state before the
+ *                                 first byte.  Positions need not be sorted or
+ *                                 distinct.  Device memory, read only.
+ *   npos   >= 0                   0 disables recording (pos and h_pos are then
+ *                                 ignored and may be NULL).
+ *   h_pos  float (npos, B, D, N)  h_pos[k][b][d][n] = h_p[n] of row (b, d)
+ *                                 after timestep p = pos[k * B + b] (h0, or
+ *                                 zeros, for p = -1).  A position outside
+ *                                 [-1, L-1] is not an error: its slot is
+ *                                 filled with NaN.  h_pos[k] has the layout of
+ *                                 h0, so it can be passed back as h0 to resume
+ *                                 every row of the batch from its k-th
+ *                                 position.  h_pos must not overlap any other
+ *                                 argument; pos must not overlap y or h_last.
+ *
+ * Every other argument is as for mb_scan_fwd, and y and h_last are the same
+ * bits as mb_scan_fwd's.  A recorded state equals the state the scan carries
+ * at that timestep bit for bit.
+ */
+int mb_scan_fwd_states(const mb_scan_desc *desc,
+                       const void *u, const void *delta, const float *A,
+                       const void *Bmat, const void *Cmat,
+                       const float *Dskip, const float *dt_bias, const void *z,
+                       const float *h0, void *y, float *h_last,
+                       const int32_t *pos, int64_t npos, float *h_pos, void *stream);
 
 /*
  * One recurrent step per row, the state updated in place (Section 2:

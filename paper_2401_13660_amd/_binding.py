@@ -45,6 +45,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib = ctypes.CDLL(path)
     lib.mb_scan_fwd.restype = ctypes.c_int
     lib.mb_scan_fwd.argtypes = [ctypes.POINTER(ScanDesc)] + [_VP] * 12
+    lib.mb_scan_fwd_states.restype = ctypes.c_int
+    lib.mb_scan_fwd_states.argtypes = [ctypes.POINTER(ScanDesc)] + [_VP] * 11 + [_VP, ctypes.c_int64, _VP, _VP]
     lib.mb_scan_step.restype = ctypes.c_int
     lib.mb_scan_step.argtypes = [ctypes.c_int64] * 3 + [ctypes.c_int32] * 3 + [_VP] * 11
     lib.mb_status_string.restype = ctypes.c_char_p
@@ -88,11 +90,17 @@ def _need(t, name, shape, dtype=None, device=None):
 
 
 def scan_fwd(u, delta, A, B, C, D=None, dt_bias=None, z=None, h0=None, *, delta_softplus=True,
-             out_dtype=torch.float32, return_last_state=False, out=None, h_last=None):
+             out_dtype=torch.float32, return_last_state=False, out=None, h_last=None,
+             positions=None, h_at=None):
     """Selective scan over (batch, dim, L) inputs; returns y or (y, h_last).
 
     u, delta, z: (batch, dim, L); B, C: (batch, N, L), all of one dtype (fp32 or bf16);
     A: (dim, N) fp32; D, dt_bias: (dim,) fp32; h0: (batch, dim, N) fp32.
+
+    ``positions``: int32 (npos, batch) on the GPU; position k of batch element b is a
+    timestep in [0, L) or -1 (the initial state).  The states there are returned as a
+    last extra element ``h_at`` of shape (npos, batch, dim, N) (NaN for a position
+    outside [-1, L-1]); ``h_at[k]`` can be passed back as ``h0`` to resume.
     """
     lib = load_library()
     if not isinstance(u, torch.Tensor) or u.dim() != 3:
@@ -123,14 +131,36 @@ def scan_fwd(u, delta, A, B, C, D=None, dt_bias=None, z=None, h0=None, *, delta_
         h_last = torch.empty((nb, dim, N), dtype=torch.float32, device=dev)
     elif h_last is not None:
         _need(h_last, "h_last", (nb, dim, N), torch.float32, dev)
+    npos = 0
+    if positions is not None:
+        if not isinstance(positions, torch.Tensor) or positions.dim() != 2:
+            raise MBScanError("positions must be an int32 (npos, batch) tensor")
+        npos = positions.shape[0]
+        _need(positions, "positions", (npos, nb), torch.int32, dev)
+        if h_at is None:
+            h_at = torch.empty((npos, nb, dim, N), dtype=torch.float32, device=dev)
+        else:
+            _need(h_at, "h_at", (npos, nb, dim, N), torch.float32, dev)
+    elif h_at is not None:
+        raise MBScanError("h_at given without positions")
     desc = ScanDesc(nb, dim, L, N, _dt(act), _dt(out.dtype), 1 if delta_softplus else 0, 0)
     stream = torch.cuda.current_stream(dev).cuda_stream
     with torch.cuda.device(dev):
-        st = lib.mb_scan_fwd(ctypes.byref(desc), _ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C),
-                             _ptr(D), _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(out), _ptr(h_last),
-                             stream)
-    _check(st, "mb_scan_fwd")
-    return (out, h_last) if (return_last_state or h_last is not None) else out
+        if positions is None:
+            st = lib.mb_scan_fwd(ctypes.byref(desc), _ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C),
+                                 _ptr(D), _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(out), _ptr(h_last),
+                                 stream)
+        else:
+            st = lib.mb_scan_fwd_states(ctypes.byref(desc), _ptr(u), _ptr(delta), _ptr(A), _ptr(B),
+                                        _ptr(C), _ptr(D), _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(out),
+                                        _ptr(h_last), _ptr(positions), npos, _ptr(h_at), stream)
+    _check(st, "mb_scan_fwd" if positions is None else "mb_scan_fwd_states")
+    res = (out,)
+    if return_last_state or h_last is not None:
+        res += (h_last,)
+    if positions is not None:
+        res += (h_at,)
+    return res[0] if len(res) == 1 else res
 
 
 def scan_step(h, u_t, delta_t, A, B_t, C_t, D=None, dt_bias=None, z_t=None, *, delta_softplus=True,

@@ -89,15 +89,17 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
         const int64_t waves = n_cg * p.batch * (nseg - 1);
         const int64_t blocks = (waves + T::kWavesPerGroup - 1) / T::kWavesPerGroup;
         void *args[] = {&p, &seg_len, &carry};
-        e = hipLaunchKernel(reinterpret_cast<const void *>(&T::scan_fwd_tiled<IN, OUT, GATE, SP, true>),
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&T::scan_fwd_tiled<IN, OUT, GATE, SP, true, false>),
                             dim3((unsigned)blocks), dim3(T::kThreads), args, lds, st);
         if (e != hipSuccess) { (void)hipFreeAsync(carry, st); return e; }
     }
     const int64_t waves = n_cg * p.batch * nseg;
     const int64_t blocks = (waves + T::kWavesPerGroup - 1) / T::kWavesPerGroup;
     void *args[] = {&p, &seg_len, &carry};
-    e = hipLaunchKernel(reinterpret_cast<const void *>(&T::scan_fwd_tiled<IN, OUT, GATE, SP, false>),
-                        dim3((unsigned)blocks), dim3(T::kThreads), args, lds, st);
+    const void *main_fn = p.npos > 0
+        ? reinterpret_cast<const void *>(&T::scan_fwd_tiled<IN, OUT, GATE, SP, false, true>)
+        : reinterpret_cast<const void *>(&T::scan_fwd_tiled<IN, OUT, GATE, SP, false, false>);
+    e = hipLaunchKernel(main_fn, dim3((unsigned)blocks), dim3(T::kThreads), args, lds, st);
     if (carry) {
         const hipError_t f = hipFreeAsync(carry, st);
         if (e == hipSuccess) e = f;
@@ -178,19 +180,31 @@ const char *mb_status_string(int status) {
 int mb_scan_fwd(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
                 const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
                 const void *z, const float *h0, void *y, float *h_last, void *stream) {
+    return mb_scan_fwd_states(desc, u, delta, A, Bmat, Cmat, Dskip, dt_bias, z, h0, y, h_last, nullptr, 0,
+                              nullptr, stream);
+}
+
+int mb_scan_fwd_states(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
+                       const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
+                       const void *z, const float *h0, void *y, float *h_last, const int32_t *pos,
+                       int64_t npos, float *h_pos, void *stream) {
     if (!desc) return MB_ERR_NULL;
     const int64_t B = desc->batch, D = desc->dim, L = desc->seqlen, N = desc->dstate;
     if (B < 0 || D < 0 || L < 0 || N < 0) return MB_ERR_SHAPE;
     if (!valid_dtype(desc->in_dtype) || !valid_dtype(desc->out_dtype)) return MB_ERR_DTYPE;
     if (desc->reserved != 0 || !supported_dstate(N)) return MB_ERR_UNSUPPORTED;
-    int64_t rows, elems, bc_elems, state_elems;
+    int64_t rows, elems, bc_elems, state_elems, pos_elems = 0, hpos_elems = 0;
+    if (npos < 0) return MB_ERR_SHAPE;
     if (!mul_ok(B, D, &rows) || !mul_ok(rows, L, &elems) || !mul_ok(B * N, L, &bc_elems) ||
-        !mul_ok(rows, N, &state_elems))
+        !mul_ok(rows, N, &state_elems) || !mul_ok(npos, B, &pos_elems) ||
+        !mul_ok(npos, state_elems, &hpos_elems))
         return MB_ERR_SHAPE;
     if (rows == 0) return MB_OK;
 
     if (!A) return MB_ERR_NULL;
     if (L > 0 && (!u || !delta || !Bmat || !Cmat || !y)) return MB_ERR_NULL;
+    if (npos > 0 && (!pos || !h_pos)) return MB_ERR_NULL;
+    if (npos > 0 && (!aligned(pos, 4) || !aligned(h_pos, 4))) return MB_ERR_ALIGN;
 
     const size_t in_sz = dtype_size(desc->in_dtype), out_sz = dtype_size(desc->out_dtype);
     const void *act[] = {u, delta, Bmat, Cmat, z};
@@ -215,6 +229,34 @@ int mb_scan_fwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     }
     if (overlaps(h_last, st_bytes, y, y_bytes)) return MB_ERR_ALIAS;
     if (h0 && h_last && h0 != h_last && overlaps(h_last, st_bytes, h0, st_bytes)) return MB_ERR_ALIAS;
+    if (npos > 0) {
+        // h_pos overlaps nothing; pos is an input like the others.
+        const size_t pos_bytes = (size_t)pos_elems * 4, hpos_bytes = (size_t)hpos_elems * 4;
+        for (const Range &r : ins)
+            if (overlaps(h_pos, hpos_bytes, r.p, r.n)) return MB_ERR_ALIAS;
+        if (overlaps(h_pos, hpos_bytes, pos, pos_bytes) || overlaps(h_pos, hpos_bytes, y, y_bytes) ||
+            overlaps(h_pos, hpos_bytes, h_last, st_bytes) || overlaps(pos, pos_bytes, y, y_bytes) ||
+            overlaps(pos, pos_bytes, h_last, st_bytes))
+            return MB_ERR_ALIAS;
+    }
+
+    ScanParams p{};
+    p.batch = B; p.dim = D; p.seqlen = L;
+    p.u = u; p.delta = delta; p.Bm = Bmat; p.Cm = Cmat; p.z = z;
+    p.A = A; p.Dskip = Dskip; p.dt_bias = dt_bias; p.h0 = h0;
+    p.y = y; p.h_last = h_last;
+    p.pos = npos > 0 ? pos : nullptr; p.npos = npos; p.h_pos = npos > 0 ? h_pos : nullptr;
+    p.delta_softplus = desc->delta_softplus ? 1 : 0;
+
+    if (npos > 0) {
+        // Position -1 and invalid positions, before h_last (which may be h0) is written.
+        const dim3 block(256), grid((unsigned)((hpos_elems + 255) / 256));
+        int64_t n_arg = N;
+        void *args[] = {&p, &n_arg};
+        const hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&mbs::init_positions), grid,
+                                             block, args, 0, static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return MB_ERR_HIP;
+    }
 
     if (L == 0) {
         if (!h_last || h_last == h0) return MB_OK;
@@ -225,13 +267,6 @@ int mb_scan_fwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
                                              args, 0, static_cast<hipStream_t>(stream));
         return e == hipSuccess ? MB_OK : MB_ERR_HIP;
     }
-
-    ScanParams p{};
-    p.batch = B; p.dim = D; p.seqlen = L;
-    p.u = u; p.delta = delta; p.Bm = Bmat; p.Cm = Cmat; p.z = z;
-    p.A = A; p.Dskip = Dskip; p.dt_bias = dt_bias; p.h0 = h0;
-    p.y = y; p.h_last = h_last;
-    p.delta_softplus = desc->delta_softplus ? 1 : 0;
 
     hipError_t e;
     if (desc->in_dtype == MB_F32)

@@ -46,11 +46,32 @@ __global__ __launch_bounds__(64) void scan_fwd_rowwise(ScanParams p) {
         float yv = __builtin_fmaf(dskip, x, acc);
         if (p.z) yv *= silu_f32(Act<IN>::ld(p.z, base + t));
         st_out<OUT>(p.y, base + t, yv);
+        for (int64_t k = 0; k < p.npos; ++k) {          // states at requested positions
+            if (p.pos[k * p.batch + b] != t) continue;
+            float *dst = p.h_pos + ((k * p.batch + b) * p.dim + d) * N;
+#pragma unroll
+            for (int n = 0; n < N; ++n) dst[n] = h[n];
+        }
     }
     if (p.h_last) {
 #pragma unroll
         for (int n = 0; n < N; ++n) p.h_last[row * N + n] = h[n];
     }
+}
+
+// The slots of h_pos the scan kernels do not write: position -1 is the state
+// before the first timestep (h0, or zeros), and a position outside
+// [-1, seqlen - 1] reads NaN.  One thread per (k, b, d, n).
+__global__ void init_positions(ScanParams p, int64_t N) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t per_k = p.batch * p.dim * N;
+    if (i >= p.npos * per_k) return;
+    const int64_t k = i / per_k;
+    const int64_t rest = i - k * per_k;                 // (b * dim + d) * N + n
+    const int64_t b = rest / (p.dim * N);
+    const int32_t pos = p.pos[k * p.batch + b];
+    if (pos == -1) p.h_pos[i] = p.h0 ? p.h0[rest] : 0.0f;
+    else if (pos < -1 || pos >= p.seqlen) p.h_pos[i] = __builtin_nanf("");
 }
 
 // seqlen == 0: the final state is the initial one.

@@ -85,7 +85,8 @@ struct WaveSmem {
 //   end state H[n]; written to carry[((seg * rows + row) * 16 + n) * 2 + {0, 1}].
 //   Folding h <- P h + H is the associative operator of the parallel-scan
 //   formulation (Section 2, "Implementation") applied across segments.
-template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool PREPASS>
+// POS = true (scan only): also record the states at p.pos (p.npos > 0).
+template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool PREPASS, bool POS>
 __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len, float *carry) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -209,6 +210,35 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     };
 
+    // States at requested positions inside the chunk at t0: starting from the
+    // state before the chunk, replay the chunk's first timesteps from the
+    // (dlt, dx) and B tables, which phase B has finished reading and the next
+    // phase A has not yet rewritten.  The replay repeats phase B's operations
+    // in the same order, so the recorded state equals the one the scan carries.
+    auto record_positions = [&](int64_t t0, int nt, float r0, float r1) {
+        for (int64_t k = 0; k < p.npos; ++k) {
+            const int64_t pk = p.pos[k * p.batch + b];              // wave-uniform
+            if (pk < t0 || pk >= t0 + nt) continue;
+            const int cnt = (int)(pk - t0) + 1;
+            float g0 = r0, g1 = r1;
+            for (int i = 0; i < cnt; ++i) {
+                const f32x4 dv = sm.dd[i >> 1][j];
+                const float dl = (i & 1) ? dv.z : dv.x;
+                const float dx = (i & 1) ? dv.w : dv.y;
+                const f32x4 bv = sm.bc[i][q];
+                const float a0 = hw_exp2(dl * a2[0]);
+                const float a1 = hw_exp2(dl * a2[1]);
+                g0 = __builtin_fmaf(a0, g0, dx * bv[0]);
+                g1 = __builtin_fmaf(a1, g1, dx * bv[1]);
+            }
+            if (live) {
+                float *dst = p.h_pos + ((k * p.batch + b) * p.dim + d) * kN + n0;
+                dst[0] = g0;
+                dst[1] = g1;
+            }
+        }
+    };
+
     auto chunk = [&](Slot &sl, int64_t t0) {
         const int nt = (int)(t_end - t0 < kT ? t_end - t0 : kT);   // valid timesteps, multiple of 16
 
@@ -239,6 +269,8 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
 
         // ---- B: the recurrence, fully unrolled over the chunk; the operands of
         //      step i + 1 are read from LDS while step i computes ----------------
+        const float hs0 = POS ? h[0] : 0.0f;        // the state before this chunk
+        const float hs1 = POS ? h[1] : 0.0f;
         {
             f32x4 ddA[2], bcA[4], ddB[2], bcB[4];
             using I0 = std::integral_constant<int, 0>;
@@ -301,6 +333,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
                 }
             }
         }
+        if (POS) record_positions(t0, nt, hs0, hs1);
         wave_sync();   // part / dd / bc are rewritten by the next chunk
     };
 

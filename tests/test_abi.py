@@ -30,14 +30,15 @@ def declared_functions():
 def test_exports_every_declared_symbol():
     lib = mb.load_library()
     names = declared_functions()
-    assert {"mb_scan_fwd", "mb_scan_step", "mb_status_string", "mb_abi_version"} <= set(names)
+    assert {"mb_scan_fwd", "mb_scan_fwd_states", "mb_scan_step", "mb_status_string",
+            "mb_abi_version"} <= set(names)
     for n in names:
         assert hasattr(lib, n), f"{n} declared in mbscan.h but not exported"
 
 
 def test_version_and_status_strings():
     lib = mb.load_library()
-    assert lib.mb_abi_version() == 1
+    assert lib.mb_abi_version() == 2
     for code in range(-7, 1):
         assert lib.mb_status_string(code)
     assert lib.mb_status_string(-99) == b"unknown status"
@@ -87,6 +88,34 @@ def _fwd(desc, **over):
 ])
 def test_fwd_rejects(desc, over, code):
     assert _fwd(desc, **over) == code
+
+
+def _fwd_states(desc, npos, **over):
+    a = dict(P, pos=0x0c000000, hpos=0x0e000000)
+    a.update(over)
+    lib = mb.load_library()
+    return lib.mb_scan_fwd_states(ctypes.byref(desc), a["u"], a["delta"], a["A"], a["B"], a["C"], a["D"],
+                                  a["bias"], a["z"], a["h0"], a["y"], a["hl"], a["pos"], npos, a["hpos"],
+                                  None)
+
+
+@no_gpu_only
+@pytest.mark.parametrize("npos,over,code", [
+    (-1, {}, -2),
+    (1 << 62, {}, -2),
+    (2, dict(pos=None), -1),
+    (2, dict(hpos=None), -1),
+    (2, dict(pos=0x0c000002), -4),                      # int32 positions need 4-byte alignment
+    (2, dict(hpos=0x0e000002), -4),
+    (2, dict(hpos=P["u"] + 256), -7),                   # h_pos inside u
+    (2, dict(hpos=P["h0"]), -7),                        # h_pos on top of h0
+    (2, dict(hpos=P["hl"]), -7),                        # h_pos on top of h_last
+    (2, dict(pos=P["y"]), -7),                          # positions inside the output
+    (2, dict(hpos=0x0c000000 - 64), -7),                # h_pos running into the positions
+    (1, dict(u=None), -1),                              # the mb_scan_fwd checks still apply
+])
+def test_fwd_states_rejects(npos, over, code):
+    assert _fwd_states(_desc(), npos, **over) == code
 
 
 @no_gpu_only
