@@ -13,8 +13,6 @@ same workload (which doubles as the parity gate).
 from __future__ import annotations
 
 import argparse
-import glob
-import hashlib
 import json
 import os
 import sys
@@ -27,16 +25,18 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
 
-# ALU roofline of the scan (derivation in the design doc section 7.1): per element the
-# method needs 16 exponentials and 64 other fp32 VALU operations for the 16-state
-# recurrence, plus at least 4 transcendentals and 12 VALU operations of
-# per-element work.  MI355X: 1024 SIMDs at 2.4 GHz; a wave64 fp32 VALU op every
-# 2 cycles (157.3 TFLOP/s), a transcendental every 8 (quarter rate).
-ALU_SIMD_CYCLES_PER_ELEMENT = (20 * 8 + 76 * 2) / 64.0
+# ALU roofline of the scan: per element the method needs 16 exponentials and 64
+# other fp32 VALU operations for the 16-state recurrence (per state: dlt * A,
+# dlt * u * B, the state FMA and the C FMA), plus at least 4 transcendentals
+# (softplus: exp, log; silu: exp, rcp) and 12 VALU operations of per-element work.
+# MI355X: 1024 SIMDs at 2.4 GHz; an fp32 VALU op at 32 lanes per clock per SIMD
+# (157.3 TFLOP/s with an FMA as 2 flops: a wave64 op every 2 cycles), a
+# transcendental at 16 lanes per clock (a wave64 op every 4 cycles).
+ALU_SIMD_CYCLES_PER_ELEMENT = (20 * 4 + 76 * 2) / 64.0
 ALU_PEAK_GELEMS = 1024 * 2.4e9 / ALU_SIMD_CYCLES_PER_ELEMENT / 1e9
 METRIC = "selective-scan GB/s & %HBM peak (972M layer, L=8192); B·L·D elems/s"
 DEFAULT_WORKLOAD = "mambabyte972m_L8192"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+from paper_2401_13660_amd.profile_summary import TRAFFIC_FILE, kernel_sources_digest  # noqa: E402
 
 
 def algorithmic_bytes(inp, out_bytes=4, want_h_last=False) -> int:
@@ -64,14 +64,6 @@ def step_bytes(inp) -> int:
     per += inp.dim * inp.dstate * 4 + inp.dim * 4 * ((inp.Dskip is not None) + (inp.dt_bias is not None))
     per += 2 * rows * inp.dstate * 4
     return int(per * inp.seqlen)
-
-
-def kernel_sources_digest() -> str:
-    h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2401_13660_amd", "csrc", "*"))):
-        with open(p, "rb") as f:
-            h.update(os.path.basename(p).encode() + f.read())
-    return h.hexdigest()[:16]
 
 
 def measured_traffic(workload: str):

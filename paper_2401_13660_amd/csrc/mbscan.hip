@@ -53,66 +53,6 @@ hipError_t fwd_rowwise(ScanParams &p, void *stream) {
                   stream);
 }
 
-// Time segments for the tiled path.  One wave covers 8 channels of one batch
-// element.  With fewer than ~0.75 such waves per SIMD (1024 SIMDs) most of the
-// chip idles, so the sequence is cut into segments (each a multiple of 32
-// bytes, at least 256) aiming at about 4 waves per SIMD.  A pre-pass computes
-// each segment's aggregate from a zero state; the scan of segment s then starts
-// from h0 folded with the aggregates of segments 0 .. s-1.  Above that
-// threshold the pre-pass costs more than the extra occupancy returns.
-int64_t choose_segments(int64_t waves_base, int64_t L, int64_t *seg_len) {
-    int64_t nseg = 1;
-    if (waves_base < 768) nseg = (4096 + waves_base - 1) / waves_base;
-    const int64_t max_seg = L / 256;
-    if (nseg > max_seg) nseg = max_seg;
-    if (nseg < 1) nseg = 1;
-    int64_t len = (L + nseg - 1) / nseg;
-    len = (len + 31) / 32 * 32;
-    *seg_len = len;
-    return (L + len - 1) / len;
-}
-
-template <int IN, int OUT, bool GATE, bool SP>
-hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
-    namespace T = mbs::tiled;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    const int64_t n_cg = (p.dim + T::kCh - 1) / T::kCh;
-    int64_t seg_len = p.seqlen;
-    const int64_t nseg = choose_segments(n_cg * p.batch, p.seqlen, &seg_len);
-    float *carry = nullptr;
-    const size_t lds = sizeof(T::WaveSmem) * T::kWavesPerGroup;
-    hipError_t e;
-    if (nseg > 1) {
-        const size_t bytes = (size_t)(nseg - 1) * (size_t)(p.batch * p.dim) * T::kN * 2 * sizeof(float);
-        e = hipMallocAsync(reinterpret_cast<void **>(&carry), bytes, st);
-        if (e != hipSuccess) return e;
-        const int64_t waves = n_cg * p.batch * (nseg - 1);
-        const int64_t blocks = (waves + T::kWavesPerGroup - 1) / T::kWavesPerGroup;
-        void *args[] = {&p, &seg_len, &carry};
-        e = hipLaunchKernel(reinterpret_cast<const void *>(&T::scan_fwd_tiled<IN, OUT, GATE, SP, true, false>),
-                            dim3((unsigned)blocks), dim3(T::kThreads), args, lds, st);
-        if (e != hipSuccess) { (void)hipFreeAsync(carry, st); return e; }
-    }
-    const int64_t waves = n_cg * p.batch * nseg;
-    const int64_t blocks = (waves + T::kWavesPerGroup - 1) / T::kWavesPerGroup;
-    void *args[] = {&p, &seg_len, &carry};
-    const void *main_fn = p.npos > 0
-        ? reinterpret_cast<const void *>(&T::scan_fwd_tiled<IN, OUT, GATE, SP, false, true>)
-        : reinterpret_cast<const void *>(&T::scan_fwd_tiled<IN, OUT, GATE, SP, false, false>);
-    e = hipLaunchKernel(main_fn, dim3((unsigned)blocks), dim3(T::kThreads), args, lds, st);
-    if (carry) {
-        const hipError_t f = hipFreeAsync(carry, st);
-        if (e == hipSuccess) e = f;
-    }
-    return e;
-}
-
-template <int IN, int OUT, bool GATE>
-hipError_t fwd_tiled(ScanParams &p, void *stream) {
-    return p.delta_softplus ? fwd_tiled_sp<IN, OUT, GATE, true>(p, stream)
-                            : fwd_tiled_sp<IN, OUT, GATE, false>(p, stream);
-}
-
 // The tiled kernel takes dstate 16 with 16-byte aligned activation rows.
 bool tiled_ok(const ScanParams &p, int64_t N, int32_t in_dtype, int32_t out_dtype) {
     // 32-bit lane offsets inside a wave's rows: (16 rows) x L x 4 bytes < 2^32
@@ -127,7 +67,8 @@ bool tiled_ok(const ScanParams &p, int64_t N, int32_t in_dtype, int32_t out_dtyp
 template <int IN, int OUT>
 hipError_t fwd_dispatch_n(ScanParams &p, int64_t N, void *stream) {
     if (tiled_ok(p, N, IN, OUT))
-        return p.z ? fwd_tiled<IN, OUT, true>(p, stream) : fwd_tiled<IN, OUT, false>(p, stream);
+        return p.z ? mbs::tiled::fwd_tiled<IN, OUT, true>(p, stream)
+                   : mbs::tiled::fwd_tiled<IN, OUT, false>(p, stream);
     switch (N) {
         case 1: return fwd_rowwise<IN, OUT, 1>(p, stream);
         case 2: return fwd_rowwise<IN, OUT, 2>(p, stream);

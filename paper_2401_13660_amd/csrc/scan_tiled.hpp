@@ -26,6 +26,8 @@
 // row-per-thread kernel).
 #pragma once
 
+#include <hip/hip_runtime.h>
+
 #include "device_math.hpp"
 #include "scan_params.hpp"
 
@@ -356,6 +358,67 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
 #pragma unroll
         for (int s = 0; s < 2; ++s) p.h_last[row * kN + n0 + s] = h[s];
     }
+}
+
+// ---- host side: launch configuration -------------------------------------
+
+// Time segments for the tiled path.  One wave covers 8 channels of one batch
+// element.  With fewer than ~0.75 such waves per SIMD (1024 SIMDs) most of the
+// chip idles, so the sequence is cut into segments (each a multiple of 32
+// bytes, at least 256) aiming at about 4 waves per SIMD.  A pre-pass computes
+// each segment's aggregate from a zero state; the scan of segment s then starts
+// from h0 folded with the aggregates of segments 0 .. s-1.  Above that
+// threshold the pre-pass costs more than the extra occupancy returns.
+inline int64_t choose_segments(int64_t waves_base, int64_t L, int64_t *seg_len) {
+    int64_t nseg = 1;
+    if (waves_base < 768) nseg = (4096 + waves_base - 1) / waves_base;
+    const int64_t max_seg = L / 256;
+    if (nseg > max_seg) nseg = max_seg;
+    if (nseg < 1) nseg = 1;
+    int64_t len = (L + nseg - 1) / nseg;
+    len = (len + 31) / 32 * 32;
+    *seg_len = len;
+    return (L + len - 1) / len;
+}
+
+template <int IN, int OUT, bool GATE, bool SP>
+hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int64_t n_cg = (p.dim + kCh - 1) / kCh;
+    int64_t seg_len = p.seqlen;
+    const int64_t nseg = choose_segments(n_cg * p.batch, p.seqlen, &seg_len);
+    float *carry = nullptr;
+    const size_t lds = sizeof(WaveSmem) * kWavesPerGroup;
+    hipError_t e;
+    if (nseg > 1) {
+        const size_t bytes = (size_t)(nseg - 1) * (size_t)(p.batch * p.dim) * kN * 2 * sizeof(float);
+        e = hipMallocAsync(reinterpret_cast<void **>(&carry), bytes, st);
+        if (e != hipSuccess) return e;
+        const int64_t waves = n_cg * p.batch * (nseg - 1);
+        const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;
+        void *args[] = {&p, &seg_len, &carry};
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, true, false>),
+                            dim3((unsigned)blocks), dim3(kThreads), args, lds, st);
+        if (e != hipSuccess) { (void)hipFreeAsync(carry, st); return e; }
+    }
+    const int64_t waves = n_cg * p.batch * nseg;
+    const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;
+    void *args[] = {&p, &seg_len, &carry};
+    const void *main_fn = p.npos > 0
+        ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, true>)
+        : reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false>);
+    e = hipLaunchKernel(main_fn, dim3((unsigned)blocks), dim3(kThreads), args, lds, st);
+    if (carry) {
+        const hipError_t f = hipFreeAsync(carry, st);
+        if (e == hipSuccess) e = f;
+    }
+    return e;
+}
+
+template <int IN, int OUT, bool GATE>
+hipError_t fwd_tiled(ScanParams &p, void *stream) {
+    return p.delta_softplus ? fwd_tiled_sp<IN, OUT, GATE, true>(p, stream)
+                            : fwd_tiled_sp<IN, OUT, GATE, false>(p, stream);
 }
 
 }  // namespace tiled
