@@ -63,6 +63,12 @@ class Oracle:
             ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
             _D, _D, _D, _D, _D, _D, _D, _I64, ctypes.c_int64, _D, _D, _D, _D,
             _I64, ctypes.c_int64, _D]
+        self.lib.mbo_conv1d_rows.restype = ctypes.c_int
+        self.lib.mbo_conv1d_rows.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                                             _D, _D, _D, _D, _D, _D]
+        self.lib.mbo_conv1d_step.restype = ctypes.c_int
+        self.lib.mbo_conv1d_step.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                                             _D, _D, _D, _D, _D]
         self.lib.mbo_max_threads.restype = ctypes.c_int
         self.lib.mbo_scan_step.restype = ctypes.c_int
         self.lib.mbo_scan_step.argtypes = [
@@ -186,6 +192,50 @@ class Oracle:
         if rc != 0:
             raise ValueError(f"oracle rejected the arguments (status {rc})")
         return y.reshape(nb, dim), h_new
+
+
+    # -- the causal depthwise convolution ---------------------------------------
+    def conv1d(self, x, w, *, bias=None, state=None, apply_silu=True, dtype: str | None = None):
+        """Causal depthwise convolution of (batch, dim, L) inputs with taps w (dim, K).
+
+        ``state`` (batch, dim, K-1) holds the K-1 inputs before x, oldest first (zeros
+        when absent).  Returns y (batch, dim, L) and the new state (batch, dim, K-1),
+        both fp64.  ``dtype="bf16"`` means x holds bf16 bit patterns.
+        """
+        x = np.asarray(x)
+        nb, dim, L = x.shape
+        w64 = to_f64(w)
+        K = w64.shape[1]
+        R = nb * dim
+        xf = np.ascontiguousarray(to_f64(x, dtype).reshape(R, L))
+        wf = np.ascontiguousarray(np.tile(w64, (nb, 1)))
+        bf = None if bias is None else np.ascontiguousarray(np.tile(to_f64(bias), nb))
+        sf = None if state is None else np.ascontiguousarray(to_f64(state).reshape(R, K - 1))
+        y = np.empty((R, L), dtype=np.float64)
+        st = np.empty((R, max(K - 1, 0)), dtype=np.float64)
+        rc = self.lib.mbo_conv1d_rows(R, L, K, int(bool(apply_silu)), _ptr(xf), _ptr(wf), _ptr(bf),
+                                      _ptr(sf), _ptr(y), _ptr(st) if K > 1 else None)
+        if rc != 0:
+            raise ValueError(f"oracle rejected the arguments (status {rc})")
+        return y.reshape(nb, dim, L), st.reshape(nb, dim, K - 1)
+
+    def conv1d_step(self, x_t, w, state, *, bias=None, apply_silu=True, dtype: str | None = None):
+        """One step for (batch, dim) inputs; returns (y_t (batch, dim), new state (batch, dim, K-1))."""
+        x_t = np.asarray(x_t)
+        nb, dim = x_t.shape
+        w64 = to_f64(w)
+        K = w64.shape[1]
+        R = nb * dim
+        xf = np.ascontiguousarray(to_f64(x_t, dtype).reshape(R))
+        wf = np.ascontiguousarray(np.tile(w64, (nb, 1)))
+        bf = None if bias is None else np.ascontiguousarray(np.tile(to_f64(bias), nb))
+        st = np.array(to_f64(state), dtype=np.float64, copy=True).reshape(R, K - 1)
+        y = np.empty(R, dtype=np.float64)
+        rc = self.lib.mbo_conv1d_step(R, K, int(bool(apply_silu)), _ptr(xf), _ptr(wf), _ptr(bf),
+                                      _ptr(st) if K > 1 else None, _ptr(y))
+        if rc != 0:
+            raise ValueError(f"oracle rejected the arguments (status {rc})")
+        return y.reshape(nb, dim), st.reshape(nb, dim, K - 1)
 
 
 _default = None

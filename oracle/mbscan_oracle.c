@@ -35,6 +35,18 @@
  * The single-step entry point is the loop body above for one t, updating h
  * in place (Section 2: the recurrence is run directly during generation).
  *
+ * The file also holds the oracle of the step upstream of the scan: the causal
+ * depthwise 1D convolution of the Mamba block (Table 8, "Pre-SSM 1D
+ * convolution"; Fig. 5, right, followed by the Swish activation; kernel size
+ * k = 4 in Table 9), with a carried state of the last k - 1 inputs so that a
+ * sequence can be resumed or decoded byte by byte:
+ *
+ *   xin(s)   = x[r][s] for s >= 0, state_in[r][k - 1 + s] for -(k-1) <= s < 0
+ *              (zeros when state_in is absent)
+ *   pre[t]   = bias[r] + sum_{i < k} w[r][i] * xin(t - (k-1) + i)
+ *   y[r][t]  = silu(pre[t]) if apply_silu else pre[t]
+ *   state_out[r][j] = xin(L - (k-1) + j)   for j < k - 1
+ *
  * Parity pinned by tests/test_oracle_pins.py (brute-force materialisation on
  * the time grid t_k = sum Delta, geometric closed form, B = 0, split
  * invariance, the eq. (4) gated-recurrence special case, the associative
@@ -206,6 +218,86 @@ int mbo_scan_step(int64_t R, int64_t N, int delta_softplus,
         /* B_t and C_t are (nbatch, N): the L = 1 case of the (nbatch, N, L) layout. */
         scan_one_row(r, 1, N, delta_softplus, u_t, delta_t, z_t, A, Dskip, dt_bias,
                      h, bidx, B_t, C_t, y_t, h, NULL, 0, NULL);
+    }
+    return MBO_OK;
+}
+
+/* ---- the causal depthwise convolution ------------------------------------ */
+
+#define MBO_MAX_K 64
+
+static void conv_one_row(int64_t r, int64_t L, int64_t K, int apply_silu,
+                         const double *x, const double *w, const double *bias,
+                         const double *state_in, double *y, double *state_out)
+{
+    /* xin(s) for s in [-(K-1), L): the carried inputs, then this row's inputs */
+    const int64_t H = K - 1;
+    for (int64_t t = 0; t < L; ++t) {
+        double pre = bias ? bias[r] : 0.0;
+        for (int64_t i = 0; i < K; ++i) {
+            const int64_t src = t - H + i;
+            double xv;
+            if (src >= 0)
+                xv = x[r * L + src];
+            else
+                xv = state_in ? state_in[r * H + (H + src)] : 0.0;
+            pre += w[r * K + i] * xv;
+        }
+        y[r * L + t] = apply_silu ? silu(pre) : pre;
+    }
+    if (state_out) {
+        for (int64_t j = 0; j < H; ++j) {
+            const int64_t src = L - H + j;
+            state_out[r * H + j] = src >= 0 ? x[r * L + src]
+                                            : (state_in ? state_in[r * H + (H + src)] : 0.0);
+        }
+    }
+}
+
+/*
+ * Convolution over R independent rows of length L.
+ *   x          : R x L       (input)
+ *   w          : R x K       (taps of each row's channel; w[.][K-1] multiplies the current input)
+ *   bias       : R           (may be NULL)
+ *   state_in   : R x (K-1)   (the K-1 inputs before x, oldest first; may be NULL: zeros)
+ *   y          : R x L       (output)
+ *   state_out  : R x (K-1)   (output, may be NULL: the last K-1 inputs)
+ */
+int mbo_conv1d_rows(int64_t R, int64_t L, int64_t K, int apply_silu,
+                    const double *x, const double *w, const double *bias,
+                    const double *state_in, double *y, double *state_out)
+{
+    if (R < 0 || L < 0 || K < 1 || K > MBO_MAX_K)
+        return MBO_ERR_ARG;
+    if (R == 0)
+        return MBO_OK;
+    if (!w || (L > 0 && (!x || !y)))
+        return MBO_ERR_ARG;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t r = 0; r < R; ++r)
+        conv_one_row(r, L, K, apply_silu, x, w, bias, state_in, y, state_out);
+    return MBO_OK;
+}
+
+/* One step: the convolution with L = 1, the state updated in place. */
+int mbo_conv1d_step(int64_t R, int64_t K, int apply_silu, const double *x_t,
+                    const double *w, const double *bias, double *state, double *y_t)
+{
+    if (R < 0 || K < 1 || K > MBO_MAX_K)
+        return MBO_ERR_ARG;
+    if (R == 0)
+        return MBO_OK;
+    if (!x_t || !w || !y_t || (K > 1 && !state))
+        return MBO_ERR_ARG;
+    for (int64_t r = 0; r < R; ++r) {
+        /* row r seen as row 0 of one-row arrays, so that the new state can go
+         * to a local buffer before it replaces the old one */
+        double next[MBO_MAX_K];
+        double *st = K > 1 ? state + r * (K - 1) : NULL;
+        conv_one_row(0, 1, K, apply_silu, x_t + r, w + r * K, bias ? bias + r : NULL, st,
+                     y_t + r, next);
+        for (int64_t j = 0; j < K - 1; ++j)
+            st[j] = next[j];
     }
     return MBO_OK;
 }

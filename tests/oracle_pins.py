@@ -334,8 +334,79 @@ def pin_states_at_positions(orc):
                 _close(hp[k, b], ref, 1e-11, f"state at position {p} (seed {seed}, k {k}, b {b})")
 
 
+# ---- the causal depthwise convolution upstream of the scan (Table 8, "Pre-SSM
+#      1D convolution"; Fig. 5, right: Swish after the convolution) -----------
+
+def _conv_case(seed, nb=2, dim=3, L=21, K=4, state=True, bias=True):
+    rng = np.random.default_rng(seed)
+    return dict(x=rng.standard_normal((nb, dim, L)), w=rng.standard_normal((dim, K)),
+                bias=rng.standard_normal(dim) if bias else None,
+                state=rng.standard_normal((nb, dim, K - 1)) if state else None)
+
+
+def _conv_library(c, apply_silu):
+    """The same convolution through numpy's 1D convolution over the carried history."""
+    x, w = c["x"], c["w"]
+    nb, dim, L = x.shape
+    K = w.shape[1]
+    hist = np.zeros((nb, dim, K - 1)) if c["state"] is None else c["state"]
+    xx = np.concatenate([hist, x], axis=2)
+    y = np.zeros_like(x)
+    for b in range(nb):
+        for d in range(dim):
+            # np.convolve flips its second argument: taps reversed give sum_i w[i] xx[t + i]
+            y[b, d] = np.convolve(xx[b, d], w[d][::-1], mode="valid")
+            if c["bias"] is not None:
+                y[b, d] += c["bias"][d]
+    if apply_silu:
+        y = y * expit(y)
+    return y, xx[..., xx.shape[2] - (K - 1):]
+
+
+def pin_conv_library(orc):
+    """Oracle convolution == numpy.convolve over [state, x], Swish by scipy's expit."""
+    for seed, kw in ((21, {}), (22, dict(state=False, bias=False)), (23, dict(K=2)), (24, dict(K=1)),
+                     (25, dict(L=2)), (26, dict(L=1, K=4))):
+        c = _conv_case(seed, **kw)
+        for act in (True, False):
+            y, st = orc.conv1d(c["x"], c["w"], bias=c["bias"], state=c["state"], apply_silu=act)
+            ry, rst = _conv_library(c, act)
+            _close(y, ry, 1e-13, f"conv seed {seed} silu={act}")
+            assert np.array_equal(st, rst), f"conv state seed {seed}: not the last K-1 inputs"
+
+
+def pin_conv_impulse(orc):
+    """A one-hot tap is a pure delay: tap K-1 gives y = x, tap 0 gives y[t] = x[t-(K-1)]."""
+    c = _conv_case(27, L=9)
+    K = c["w"].shape[1]
+    xx = np.concatenate([c["state"], c["x"]], axis=2)
+    for tap, ref in ((K - 1, c["x"]), (0, xx[..., : c["x"].shape[2]])):
+        w = np.zeros_like(c["w"])
+        w[:, tap] = 1.0
+        y, _ = orc.conv1d(c["x"], w, state=c["state"], apply_silu=False)
+        assert np.array_equal(y, ref), f"one-hot tap {tap} is not a delay of {K - 1 - tap}"
+
+
+def pin_conv_split_and_step(orc):
+    """Resume: conv over [0, L) == conv over [0, k) then [k, L) from its state; and L
+    single steps == one call."""
+    c = _conv_case(28, L=17)
+    y, st = orc.conv1d(c["x"], c["w"], bias=c["bias"], state=c["state"])
+    for k in (1, 2, 3, 8, 16):
+        y1, s1 = orc.conv1d(c["x"][..., :k], c["w"], bias=c["bias"], state=c["state"])
+        y2, s2 = orc.conv1d(c["x"][..., k:], c["w"], bias=c["bias"], state=s1)
+        assert np.array_equal(np.concatenate([y1, y2], axis=2), y), f"conv split at {k}"
+        assert np.array_equal(s2, st), f"conv state after split at {k}"
+    state = c["state"].copy()
+    for t in range(c["x"].shape[2]):
+        yt, state = orc.conv1d_step(c["x"][..., t], c["w"], state, bias=c["bias"])
+        assert np.array_equal(yt, y[..., t]), f"conv step {t}"
+    assert np.array_equal(state, st), "conv state after steps"
+
+
 ALL_PINS = [
     pin_golden_decimal, pin_bruteforce, pin_geometric, pin_B_zero, pin_split, pin_eq4,
     pin_tuple_scan, pin_separability, pin_linearity, pin_step_equals_fwd, pin_limits,
     pin_softplus_extremes, pin_states_at_positions,
+    pin_conv_library, pin_conv_impulse, pin_conv_split_and_step,
 ]

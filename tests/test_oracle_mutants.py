@@ -50,6 +50,15 @@ MUTANTS = [
      "record_states(t + 1, L, N, h, row_pos, P, row_out);"),
     ("position_initial_dropped", "record_states(-1, L, N, h, row_pos, P, row_out);", ""),
     ("position_invalid_zero", "out[k * N + n] = NAN;", "out[k * N + n] = 0.0;"),
+    ("conv_bias_dropped", "double pre = bias ? bias[r] : 0.0;", "double pre = 0.0;"),
+    ("conv_taps_reversed", "pre += w[r * K + i] * xv;", "pre += w[r * K + (K - 1 - i)] * xv;"),
+    ("conv_state_ignored", "xv = state_in ? state_in[r * H + (H + src)] : 0.0;", "xv = 0.0;"),
+    ("conv_state_reversed", "xv = state_in ? state_in[r * H + (H + src)] : 0.0;",
+     "xv = state_in ? state_in[r * H + (-1 - src)] : 0.0;"),
+    ("conv_state_out_shifted", "state_out[r * H + j] = src >= 0 ? x[r * L + src]",
+     "state_out[r * H + j] = src >= 0 ? x[r * L + (src > 0 ? src - 1 : 0)]"),
+    ("conv_no_silu", "y[r * L + t] = apply_silu ? silu(pre) : pre;", "y[r * L + t] = pre;"),
+    ("conv_silu_always", "y[r * L + t] = apply_silu ? silu(pre) : pre;", "y[r * L + t] = silu(pre);"),
     ("last_state_dropped_from_y", "for (int64_t n = 0; n < N; ++n) {\n            const double abar",
      "for (int64_t n = 0; n < N; ++n) {\n            if (n == N - 1 && N > 1) continue;\n            const double abar"),
 ]
