@@ -36,7 +36,8 @@ ALU_SIMD_CYCLES_PER_ELEMENT = (20 * 4 + 76 * 2) / 64.0
 ALU_PEAK_GELEMS = 1024 * 2.4e9 / ALU_SIMD_CYCLES_PER_ELEMENT / 1e9
 METRIC = "selective-scan GB/s & %HBM peak (972M layer, L=8192); B·L·D elems/s"
 DEFAULT_WORKLOAD = "mambabyte972m_L8192"
-from paper_2401_13660_amd.profile_summary import TRAFFIC_FILE, kernel_sources_digest  # noqa: E402
+from paper_2401_13660_amd.profile_summary import (  # noqa: E402
+    CONV_KERNEL_SOURCES, KERNEL_SOURCES, TRAFFIC_FILE, kernel_sources_digest)
 
 
 def algorithmic_bytes(inp, out_bytes=4, want_h_last=False) -> int:
@@ -66,7 +67,7 @@ def step_bytes(inp) -> int:
     return int(per * inp.seqlen)
 
 
-def measured_traffic(workload: str):
+def measured_traffic(workload: str, sources=KERNEL_SOURCES):
     """HBM bytes per launch from the committed rocprofv3 PMC summary, if it was
     taken on the current kernel sources (else None)."""
     try:
@@ -74,7 +75,7 @@ def measured_traffic(workload: str):
             rec = json.load(f).get(workload)
     except (OSError, ValueError):
         return None
-    if not rec or rec.get("kernel_sources") != kernel_sources_digest():
+    if not rec or rec.get("kernel_sources") != kernel_sources_digest(sources):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -102,6 +103,90 @@ def cpu_baseline(inp, y_gpu):
                 parity_ok=worst <= TOL_Y)
 
 
+def conv_bytes(c, out_bytes=2) -> int:
+    """Each input read once and each output written once (the roofline's bytes)."""
+    act = 2 if c.dtype == "bf16" else 4
+    E = c.batch * c.dim * c.seqlen
+    b = E * (act + out_bytes) + c.dim * c.width * 4 + (c.dim * 4 if c.bias is not None else 0)
+    st = c.batch * c.dim * (c.width - 1) * 4
+    return int(b + st * (1 + (c.state is not None)))
+
+
+def bench_conv(args):
+    """One mb_conv1d_fwd per step over the named workload's (batch, dim, L): the
+    convolution + Swish whose bf16 output is the scan's u (and x_proj's input)."""
+    import torch
+
+    import paper_2401_13660_amd as mb
+    from paper_2401_13660_amd.inputs import WORKLOADS, conv_workload
+
+    c = conv_workload(args.workload, seed=0)
+    dev = torch.device("cuda:0")
+
+    def t(a):
+        if a is None:
+            return None
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    x, w, bias, state = t(c.x), t(c.w), t(c.bias), t(c.state)
+    y = torch.empty_like(x, dtype=torch.bfloat16)
+    state_out = torch.empty((c.batch, c.dim, c.width - 1), dtype=torch.float32, device=dev)
+
+    def step():
+        mb.conv1d(x, w, bias=bias, state=state, out=y, state_out=state_out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    E = c.batch * c.dim * c.seqlen
+    nbytes = conv_bytes(c)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    line = {
+        "metric": "causal-conv1d GB/s & %HBM peak (in front of the scan); B·L·D elems/s",
+        "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": args.workload, "mode": "conv", "width": c.width,
+                   **{k: v for k, v in WORKLOADS[args.workload].items() if k != "dstate"},
+                   "state": c.state is not None, "out_dtype": "bf16", "parallelism": "single GPU"},
+        "elems_per_s": round(E / (ms * 1e-3), 1),
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic("conv:" + args.workload, CONV_KERNEL_SOURCES),
+                     "algorithmic_bytes": nbytes},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        from parity import rel_err
+
+        orc = oracle.default()
+        t0 = time.perf_counter()
+        y_ref, st_ref = orc.conv1d(c.x, c.w, bias=c.bias, state=c.state, dtype=c.dtype)
+        elapsed = time.perf_counter() - t0
+        err = rel_err(y.float().cpu().numpy(), y_ref)
+        ok = err <= 1e-5 + 2.0 ** -8 and np.array_equal(state_out.cpu().numpy().astype(np.float64), st_ref)
+        line["cpu_baseline"] = {
+            "value": round(nbytes / elapsed / 1e9, 3), "unit": "GB/s", "elems_per_s": round(E / elapsed, 1),
+            "cores": orc.max_threads(), "kind": "oracle",
+            "sample": f"whole workload: {c.batch} x {c.dim} rows of L={c.seqlen}, fp64, {elapsed:.1f} s"}
+        line["parity"] = {"y_rel_err_vs_oracle": err, "ok": bool(ok)}
+        if not ok:
+            print(json.dumps(line))
+            print("parity gate failed: GPU output disagrees with the oracle", file=sys.stderr)
+            sys.exit(1)
+    print(json.dumps(line))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -109,9 +194,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["fwd", "step"], default="fwd",
+    ap.add_argument("--mode", choices=["fwd", "step", "conv"], default="fwd",
                     help="fwd: one mb_scan_fwd per step; step: seqlen successive mb_scan_step calls per step "
-                         "(the recurrent-generation form of the same workload)")
+                         "(the recurrent-generation form of the same workload); conv: one mb_conv1d_fwd "
+                         "(the causal convolution + Swish in front of the scan, k = 4, bf16 out)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the scan, run a plain device copy of MIB MiB (reference for HBM counters)")
     args = ap.parse_args()
@@ -135,6 +221,9 @@ def main():
 
     import paper_2401_13660_amd as mb
     from paper_2401_13660_amd.inputs import WORKLOADS, workload
+
+    if args.mode == "conv":
+        return bench_conv(args)
 
     inp = workload(args.workload, seed=0)
     dev = torch.device("cuda:0")

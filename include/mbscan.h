@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define MB_ABI_VERSION 2
+#define MB_ABI_VERSION 3
 
 typedef enum {
     MB_F32 = 0,
@@ -60,7 +60,8 @@ typedef enum {
     MB_ERR_SHAPE = -2,       /* a size is negative or too large */
     MB_ERR_DTYPE = -3,       /* in_dtype or out_dtype is not an mb_dtype */
     MB_ERR_ALIGN = -4,       /* a pointer is not aligned to its element size */
-    MB_ERR_UNSUPPORTED = -5, /* dstate not in {1, 2, 4, 8, 16}, or a reserved field is set */
+    MB_ERR_UNSUPPORTED = -5, /* dstate not in {1, 2, 4, 8, 16}, a convolution width outside
+                                1 .. 4, or a reserved field is set */
     MB_ERR_HIP = -6,         /* the HIP runtime reported an error when launching */
     MB_ERR_ALIAS = -7        /* an output overlaps an input it may not overlap */
 } mb_status;
@@ -157,6 +158,65 @@ int mb_scan_step(int64_t batch, int64_t dim, int64_t dstate,
                  const void *B_t, const void *C_t,
                  const float *Dskip, const float *dt_bias, const void *z_t,
                  float *h, void *y_t, void *stream);
+
+/*
+ * The causal depthwise convolution upstream of the scan.  In the Mamba block
+ * the x branch is convolved per channel over time with a short kernel and a
+ * bias, then passed through the Swish activation, and the result is the scan's
+ * input u (Table 8, "Pre-SSM 1D convolution"; Fig. 5, right; kernel size
+ * k = 4 in every MambaByte model, Table 9):
+ *
+ *   pre_t = bias[d] + sum_{i < k} w[d][i] x_{t-(k-1)+i}
+ *   y_t   = pre_t * sigmoid(pre_t)     (apply_silu != 0), else pre_t
+ *
+ * The k - 1 inputs before the first byte come from a carried state, so that a
+ * sequence continues exactly where the previous call stopped, and the call
+ * returns the last k - 1 inputs as the next state (the convolution's part of
+ * the resume that Algorithm 1 relies on).  Arithmetic is fp32.
+ */
+typedef struct {
+    int64_t batch;          /* B */
+    int64_t dim;            /* D: channels (e * d) */
+    int64_t seqlen;         /* L */
+    int32_t width;          /* k: taps per channel, 1 .. 4 */
+    int32_t in_dtype;       /* mb_dtype of x */
+    int32_t out_dtype;      /* mb_dtype of y */
+    int32_t apply_silu;     /* nonzero: Swish after the convolution */
+    int32_t reserved;       /* must be 0 */
+    int32_t reserved2;      /* must be 0 */
+} mb_conv_desc;
+
+/*
+ *   x          act   (B, D, L)    input, time contiguous
+ *   w          float (D, k)       taps; w[d][k-1] multiplies the current byte
+ *   bias       float (D)          NULL means 0
+ *   state_in   float (B, D, k-1)  the k-1 inputs before x, oldest first; NULL
+ *                                 means zeros (the start of a sequence)
+ *   y          out   (B, D, L)    output; must not overlap any other argument
+ *   state_out  float (B, D, k-1)  the last k-1 inputs (of state_in followed by
+ *                                 x); NULL means not written.  It must not
+ *                                 overlap any other argument, state_in
+ *                                 included: alternate two buffers to chain
+ *                                 calls.  With L = 0 it receives state_in.
+ * Errors as for mb_scan_fwd; a width outside 1 .. 4 or a nonzero reserved
+ * field is MB_ERR_UNSUPPORTED.
+ */
+int mb_conv1d_fwd(const mb_conv_desc *desc, const void *x, const float *w, const float *bias,
+                  const float *state_in, void *y, float *state_out, void *stream);
+
+/*
+ * One byte per row, the convolution state updated in place (generation, and
+ * Algorithm 1's byte-level correction loop).  Identical to mb_conv1d_fwd with
+ * L = 1, state_in = the old state and state_out = the new one.
+ *
+ *   x_t    act   (B, D)        this byte's input
+ *   w      float (D, k), bias float (D) (NULL means 0)
+ *   state  float (B, D, k-1)   read then overwritten; required when k > 1
+ *   y_t    out   (B, D)        must not overlap any other argument
+ */
+int mb_conv1d_step(int64_t batch, int64_t dim, int32_t width, int32_t in_dtype, int32_t out_dtype,
+                   int32_t apply_silu, const void *x_t, const float *w, const float *bias,
+                   float *state, void *y_t, void *stream);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char *mb_status_string(int status);

@@ -30,6 +30,12 @@ class ScanDesc(ctypes.Structure):
                 ("delta_softplus", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+class ConvDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int64), ("dim", ctypes.c_int64), ("seqlen", ctypes.c_int64),
+                ("width", ctypes.c_int32), ("in_dtype", ctypes.c_int32), ("out_dtype", ctypes.c_int32),
+                ("apply_silu", ctypes.c_int32), ("reserved", ctypes.c_int32), ("reserved2", ctypes.c_int32)]
+
+
 _lib = None
 _VP = ctypes.c_void_p
 
@@ -49,6 +55,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mb_scan_fwd_states.argtypes = [ctypes.POINTER(ScanDesc)] + [_VP] * 11 + [_VP, ctypes.c_int64, _VP, _VP]
     lib.mb_scan_step.restype = ctypes.c_int
     lib.mb_scan_step.argtypes = [ctypes.c_int64] * 3 + [ctypes.c_int32] * 3 + [_VP] * 11
+    lib.mb_conv1d_fwd.restype = ctypes.c_int
+    lib.mb_conv1d_fwd.argtypes = [ctypes.POINTER(ConvDesc)] + [_VP] * 7
+    lib.mb_conv1d_step.restype = ctypes.c_int
+    lib.mb_conv1d_step.argtypes = [ctypes.c_int64] * 2 + [ctypes.c_int32] * 4 + [_VP] * 6
     lib.mb_status_string.restype = ctypes.c_char_p
     lib.mb_status_string.argtypes = [ctypes.c_int]
     lib.mb_abi_version.restype = ctypes.c_int
@@ -193,4 +203,72 @@ def scan_step(h, u_t, delta_t, A, B_t, C_t, D=None, dt_bias=None, z_t=None, *, d
                               _ptr(u_t), _ptr(delta_t), _ptr(A), _ptr(B_t), _ptr(C_t), _ptr(D),
                               _ptr(dt_bias), _ptr(z_t), _ptr(h), _ptr(out), stream)
     _check(st, "mb_scan_step")
+    return out
+
+
+def conv1d(x, w, bias=None, state=None, *, apply_silu=True, out_dtype=None, return_state=False,
+           out=None, state_out=None):
+    """Causal depthwise convolution (+ Swish) of x (batch, dim, L) with taps w (dim, k).
+
+    bias: (dim,) fp32; state: (batch, dim, k-1) fp32, the k-1 inputs before x (zeros when
+    None).  Returns y, or (y, state_out) where state_out holds the last k-1 inputs.
+    """
+    lib = load_library()
+    if not isinstance(x, torch.Tensor) or x.dim() != 3:
+        raise MBScanError("x must be a (batch, dim, L) tensor")
+    nb, dim, L = x.shape
+    if not isinstance(w, torch.Tensor) or w.dim() != 2:
+        raise MBScanError("w must be a (dim, k) tensor")
+    K = w.shape[1]
+    dev = x.device
+    _need(x, "x", (nb, dim, L), None, dev)
+    _need(w, "w", (dim, K), torch.float32, dev)
+    if bias is not None:
+        _need(bias, "bias", (dim,), torch.float32, dev)
+    if state is not None:
+        _need(state, "state", (nb, dim, K - 1), torch.float32, dev)
+    if out is None:
+        out = torch.empty((nb, dim, L), dtype=out_dtype or x.dtype, device=dev)
+    else:
+        _need(out, "out", (nb, dim, L), None, dev)
+    if return_state and state_out is None:
+        state_out = torch.empty((nb, dim, max(K - 1, 0)), dtype=torch.float32, device=dev)
+    elif state_out is not None:
+        _need(state_out, "state_out", (nb, dim, K - 1), torch.float32, dev)
+    desc = ConvDesc(nb, dim, L, K, _dt(x.dtype), _dt(out.dtype), 1 if apply_silu else 0, 0, 0)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    with torch.cuda.device(dev):
+        st = lib.mb_conv1d_fwd(ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(bias), _ptr(state), _ptr(out),
+                               _ptr(state_out) if K > 1 else None, stream)
+    _check(st, "mb_conv1d_fwd")
+    return (out, state_out) if (return_state or state_out is not None) else out
+
+
+def conv1d_step(state, x_t, w, bias=None, *, apply_silu=True, out_dtype=None, out=None):
+    """One byte of the convolution; state (batch, dim, k-1) fp32 is updated in place.
+    Returns y_t (batch, dim)."""
+    lib = load_library()
+    if not isinstance(x_t, torch.Tensor) or x_t.dim() != 2:
+        raise MBScanError("x_t must be a (batch, dim) tensor")
+    nb, dim = x_t.shape
+    if not isinstance(w, torch.Tensor) or w.dim() != 2:
+        raise MBScanError("w must be a (dim, k) tensor")
+    K = w.shape[1]
+    dev = x_t.device
+    _need(x_t, "x_t", (nb, dim), None, dev)
+    _need(w, "w", (dim, K), torch.float32, dev)
+    if bias is not None:
+        _need(bias, "bias", (dim,), torch.float32, dev)
+    if K > 1:
+        _need(state, "state", (nb, dim, K - 1), torch.float32, dev)
+    if out is None:
+        out = torch.empty((nb, dim), dtype=out_dtype or x_t.dtype, device=dev)
+    else:
+        _need(out, "out", (nb, dim), None, dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    with torch.cuda.device(dev):
+        st = lib.mb_conv1d_step(nb, dim, K, _dt(x_t.dtype), _dt(out.dtype), 1 if apply_silu else 0,
+                                _ptr(x_t), _ptr(w), _ptr(bias), _ptr(state) if K > 1 else None,
+                                _ptr(out), stream)
+    _check(st, "mb_conv1d_step")
     return out

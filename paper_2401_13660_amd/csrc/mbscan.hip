@@ -6,6 +6,7 @@
 
 #include <stdint.h>
 
+#include "conv1d.hpp"
 #include "mbscan.h"
 #include "scan_params.hpp"
 #include "scan_rowwise.hpp"
@@ -98,6 +99,53 @@ hipError_t step_dispatch_n(StepParams &p, int64_t N, void *stream) {
     }
 }
 
+template <int IN, int OUT, int K>
+hipError_t conv_fwd_k(mbs::conv::ConvParams &p, bool vec, void *stream) {
+    namespace C = mbs::conv;
+    const int64_t nspan = (p.seqlen + C::kSpan - 1) / C::kSpan;
+    const dim3 block(C::kThreads);
+    if (vec) {
+        uint32_t ns = (uint32_t)nspan, total = (uint32_t)(p.batch * p.dim * nspan);
+        const int64_t per_block = C::kThreads * C::kVecPerThread;
+        const dim3 grid((unsigned)((total + per_block - 1) / per_block));
+        void *args[] = {&p, &ns, &total};
+        return hipLaunchKernel(reinterpret_cast<const void *>(&C::conv1d_fwd_vec<IN, OUT, K>), grid, block,
+                               args, 0, static_cast<hipStream_t>(stream));
+    }
+    uint32_t per_row = (uint32_t)((nspan + C::kThreads - 1) / C::kThreads);
+    const dim3 grid((unsigned)(p.batch * p.dim * (int64_t)per_row));
+    void *args[] = {&p, &per_row};
+    return hipLaunchKernel(reinterpret_cast<const void *>(&C::conv1d_fwd<IN, OUT, K>), grid, block, args, 0,
+                           static_cast<hipStream_t>(stream));
+}
+
+template <int IN, int OUT, int K>
+hipError_t conv_step_k(mbs::conv::ConvParams &p, void *stream) {
+    namespace C = mbs::conv;
+    const int64_t rows = p.batch * p.dim;
+    const dim3 block(C::kThreads), grid((unsigned)((rows + C::kThreads - 1) / C::kThreads));
+    return launch(reinterpret_cast<const void *>(&C::conv1d_step<IN, OUT, K>), grid, block, &p, stream);
+}
+
+template <int IN, int OUT>
+hipError_t conv_dispatch(mbs::conv::ConvParams &p, int K, bool step, bool vec, void *stream) {
+    switch (K) {
+        case 1: return step ? conv_step_k<IN, OUT, 1>(p, stream) : conv_fwd_k<IN, OUT, 1>(p, vec, stream);
+        case 2: return step ? conv_step_k<IN, OUT, 2>(p, stream) : conv_fwd_k<IN, OUT, 2>(p, vec, stream);
+        case 3: return step ? conv_step_k<IN, OUT, 3>(p, stream) : conv_fwd_k<IN, OUT, 3>(p, vec, stream);
+        default: return step ? conv_step_k<IN, OUT, 4>(p, stream) : conv_fwd_k<IN, OUT, 4>(p, vec, stream);
+    }
+}
+
+hipError_t conv_launch(mbs::conv::ConvParams &p, int32_t in_dtype, int32_t out_dtype, int K, bool step,
+                       bool vec, void *stream) {
+    if (in_dtype == MB_F32)
+        return out_dtype == MB_F32 ? conv_dispatch<0, 0>(p, K, step, vec, stream)
+                                   : conv_dispatch<0, 1>(p, K, step, vec, stream);
+    return out_dtype == MB_F32 ? conv_dispatch<1, 0>(p, K, step, vec, stream)
+                               : conv_dispatch<1, 1>(p, K, step, vec, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -111,7 +159,7 @@ const char *mb_status_string(int status) {
         case MB_ERR_SHAPE: return "a size is negative or too large";
         case MB_ERR_DTYPE: return "unknown element type";
         case MB_ERR_ALIGN: return "a pointer is not aligned to its element size";
-        case MB_ERR_UNSUPPORTED: return "unsupported dstate or reserved field set";
+        case MB_ERR_UNSUPPORTED: return "unsupported dstate or convolution width, or reserved field set";
         case MB_ERR_HIP: return "the HIP runtime failed to launch a kernel";
         case MB_ERR_ALIAS: return "an output overlaps an input";
         default: return "unknown status";
@@ -214,6 +262,86 @@ int mb_scan_fwd_states(const mb_scan_desc *desc, const void *u, const void *delt
         e = desc->out_dtype == MB_F32 ? fwd_dispatch_n<0, 0>(p, N, stream) : fwd_dispatch_n<0, 1>(p, N, stream);
     else
         e = desc->out_dtype == MB_F32 ? fwd_dispatch_n<1, 0>(p, N, stream) : fwd_dispatch_n<1, 1>(p, N, stream);
+    return e == hipSuccess ? MB_OK : MB_ERR_HIP;
+}
+
+int mb_conv1d_fwd(const mb_conv_desc *desc, const void *x, const float *w, const float *bias,
+                  const float *state_in, void *y, float *state_out, void *stream) {
+    if (!desc) return MB_ERR_NULL;
+    const int64_t B = desc->batch, D = desc->dim, L = desc->seqlen, K = desc->width;
+    if (B < 0 || D < 0 || L < 0) return MB_ERR_SHAPE;
+    if (!valid_dtype(desc->in_dtype) || !valid_dtype(desc->out_dtype)) return MB_ERR_DTYPE;
+    if (K < 1 || K > mbs::conv::kMaxK || desc->reserved != 0 || desc->reserved2 != 0) return MB_ERR_UNSUPPORTED;
+    int64_t rows, elems, st_elems;
+    if (!mul_ok(B, D, &rows) || !mul_ok(rows, L, &elems) || !mul_ok(rows, K - 1, &st_elems))
+        return MB_ERR_SHAPE;
+    if (rows == 0) return MB_OK;
+    if (!w) return MB_ERR_NULL;
+    if (L > 0 && (!x || !y)) return MB_ERR_NULL;
+    const size_t in_sz = dtype_size(desc->in_dtype), out_sz = dtype_size(desc->out_dtype);
+    if ((x && !aligned(x, in_sz)) || (y && !aligned(y, out_sz))) return MB_ERR_ALIGN;
+    const void *f32s[] = {w, bias, state_in, state_out};
+    for (const void *q : f32s)
+        if (q && !aligned(q, 4)) return MB_ERR_ALIGN;
+    // Outputs overlap nothing (state_out may not even be state_in: the span that
+    // writes it is not the one that reads state_in).
+    const size_t x_bytes = (size_t)elems * in_sz, y_bytes = (size_t)elems * out_sz;
+    const size_t st_bytes = (size_t)st_elems * 4;
+    struct Range { const void *p; size_t n; } ins[] = {
+        {x, x_bytes}, {w, (size_t)(D * K) * 4}, {bias, (size_t)D * 4}, {state_in, st_bytes}};
+    for (const Range &r : ins)
+        if (overlaps(y, y_bytes, r.p, r.n) || overlaps(state_out, st_bytes, r.p, r.n)) return MB_ERR_ALIAS;
+    if (overlaps(y, y_bytes, state_out, st_bytes)) return MB_ERR_ALIAS;
+
+    mbs::conv::ConvParams p{};
+    p.batch = B; p.dim = D; p.seqlen = L;
+    p.x = x; p.w = w; p.bias = bias; p.state_in = state_in; p.y = y; p.state_out = state_out;
+    p.apply_silu = desc->apply_silu ? 1 : 0;
+    hipError_t e;
+    if (L == 0) {
+        // nothing to convolve: the next state is the carried one (or zeros)
+        if (!state_out || K == 1) return MB_OK;
+        void *args[] = {&p.state_in, &p.state_out, &st_elems};
+        const dim3 block(256), grid((unsigned)((st_elems + 255) / 256));
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&mbs::copy_state), grid, block, args, 0,
+                            static_cast<hipStream_t>(stream));
+        return e == hipSuccess ? MB_OK : MB_ERR_HIP;
+    }
+    // 32-bit span and block indices: rows * ceil(L / 8) spans below 2^31
+    const int64_t nspan = (L + mbs::conv::kSpan - 1) / mbs::conv::kSpan;
+    if (nspan > (int64_t(1) << 31) / rows) return MB_ERR_SHAPE;
+    const bool vec = L % mbs::conv::kSpan == 0 && aligned(x, 16) && aligned(y, 16);
+    e = conv_launch(p, desc->in_dtype, desc->out_dtype, (int)K, false, vec, stream);
+    return e == hipSuccess ? MB_OK : MB_ERR_HIP;
+}
+
+int mb_conv1d_step(int64_t batch, int64_t dim, int32_t width, int32_t in_dtype, int32_t out_dtype,
+                   int32_t apply_silu, const void *x_t, const float *w, const float *bias, float *state,
+                   void *y_t, void *stream) {
+    if (batch < 0 || dim < 0) return MB_ERR_SHAPE;
+    if (!valid_dtype(in_dtype) || !valid_dtype(out_dtype)) return MB_ERR_DTYPE;
+    if (width < 1 || width > mbs::conv::kMaxK) return MB_ERR_UNSUPPORTED;
+    int64_t rows, st_elems;
+    if (!mul_ok(batch, dim, &rows) || !mul_ok(rows, width - 1, &st_elems)) return MB_ERR_SHAPE;
+    if (rows == 0) return MB_OK;
+    if (!x_t || !w || !y_t || (width > 1 && !state)) return MB_ERR_NULL;
+    const size_t in_sz = dtype_size(in_dtype), out_sz = dtype_size(out_dtype);
+    if (!aligned(x_t, in_sz) || !aligned(y_t, out_sz)) return MB_ERR_ALIGN;
+    const void *f32s[] = {w, bias, state};
+    for (const void *q : f32s)
+        if (q && !aligned(q, 4)) return MB_ERR_ALIGN;
+    const size_t st_bytes = (size_t)st_elems * 4, y_bytes = (size_t)rows * out_sz;
+    struct Range { const void *p; size_t n; } ins[] = {
+        {x_t, (size_t)rows * in_sz}, {w, (size_t)(dim * width) * 4}, {bias, (size_t)dim * 4}};
+    for (const Range &r : ins)
+        if (overlaps(y_t, y_bytes, r.p, r.n) || overlaps(state, st_bytes, r.p, r.n)) return MB_ERR_ALIAS;
+    if (overlaps(y_t, y_bytes, state, st_bytes)) return MB_ERR_ALIAS;
+
+    mbs::conv::ConvParams p{};
+    p.batch = batch; p.dim = dim; p.seqlen = 1;
+    p.x = x_t; p.w = w; p.bias = bias; p.state_in = state; p.y = y_t; p.state_out = state;
+    p.apply_silu = apply_silu ? 1 : 0;
+    const hipError_t e = conv_launch(p, in_dtype, out_dtype, width, true, false, stream);
     return e == hipSuccess ? MB_OK : MB_ERR_HIP;
 }
 

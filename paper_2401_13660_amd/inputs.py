@@ -23,6 +23,12 @@ tensors stand in for -- the scan's cost does not depend on the data):
 Every tensor draws from its own child stream of ``SeedSequence(seed)`` (in the
 order u, Delta_raw, z, B, C, dt, Dskip, h0, A), in fixed chunks, so a tensor's
 values do not depend on which other tensors are requested.
+
+The causal convolution upstream of the scan (``make_conv_inputs``) gets its own
+streams: x ~ N(0, 1) (bf16 or fp32, shape (batch, dim, seqlen)); taps and bias
+~ U[-1/sqrt(k), 1/sqrt(k)] (the default initialisation of a depthwise Conv1d
+with fan-in k; k = 4 as in Table 9); a carried state of k - 1 earlier inputs,
+drawn like x (bf16-exact values) and held as fp32.
 """
 from __future__ import annotations
 
@@ -34,7 +40,8 @@ import numpy as np
 _CHUNK = 1 << 24
 
 # Stream indices of the child generators; fixed forever so that seeds are stable.
-_STREAMS = ("u", "delta", "z", "B", "C", "dt", "Dskip", "h0", "A")
+_STREAMS = ("u", "delta", "z", "B", "C", "dt", "Dskip", "h0", "A",
+            "conv_x", "conv_w", "conv_bias", "conv_state")
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -152,3 +159,51 @@ def workload(name: str, seed: int = 0, **overrides) -> ScanInputs:
     cfg = dict(WORKLOADS[name])
     cfg.update(overrides)
     return make_inputs(**cfg, seed=seed)
+
+
+@dataclass
+class ConvInputs:
+    """One seeded convolution workload.  bf16 tensors are uint16 bit patterns."""
+
+    batch: int
+    dim: int
+    seqlen: int
+    width: int
+    dtype: str                      # "bf16" or "f32" for x
+    x: np.ndarray
+    w: np.ndarray
+    bias: np.ndarray | None
+    state: np.ndarray | None
+    meta: dict = field(default_factory=dict)
+
+    def arrays(self) -> dict:
+        names = ("x", "w", "bias", "state")
+        return {k: getattr(self, k) for k in names if getattr(self, k) is not None}
+
+
+def make_conv_inputs(batch: int, dim: int, seqlen: int, width: int = 4, *, dtype: str = "bf16",
+                     seed: int = 0, with_bias: bool = True, with_state: bool = False) -> ConvInputs:
+    """Draw one convolution workload following the recipe in the module docstring."""
+    if dtype not in ("bf16", "f32"):
+        raise ValueError(f"dtype must be 'bf16' or 'f32', got {dtype!r}")
+    if min(batch, dim, width) < 1 or seqlen < 0:
+        raise ValueError("batch, dim, width must be >= 1 and seqlen >= 0")
+    x = _activation(_rng(seed, "conv_x"), (batch, dim, seqlen), dtype)
+    bound = 1.0 / np.sqrt(width)
+    w = _rng(seed, "conv_w").uniform(-bound, bound, size=(dim, width)).astype(np.float32)
+    bias = _rng(seed, "conv_bias").uniform(-bound, bound, size=dim).astype(np.float32) if with_bias else None
+    state = None
+    if with_state:
+        st = _normal_f32(_rng(seed, "conv_state"), (batch, dim, width - 1))
+        state = bf16_bits_to_f32(f32_to_bf16_bits(st)).reshape(st.shape) if dtype == "bf16" else st
+    return ConvInputs(batch, dim, seqlen, width, dtype, x, w, bias, state,
+                      meta=dict(seed=seed, with_state=with_state))
+
+
+def conv_workload(name: str, seed: int = 0, width: int = 4, **overrides) -> ConvInputs:
+    """The convolution in front of the scan of a named workload (same batch, dim, L, dtype)."""
+    cfg = dict(WORKLOADS[name])
+    conv = dict(batch=cfg["batch"], dim=cfg["dim"], seqlen=cfg["seqlen"], dtype=cfg["dtype"],
+                with_state=bool(cfg.get("with_h0", False)))
+    conv.update(overrides)
+    return make_conv_inputs(**conv, width=width, seed=seed)

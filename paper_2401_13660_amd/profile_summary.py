@@ -29,13 +29,15 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(_PKG)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
-# The files that define the tiled scan kernel and its launch configuration.
+# The files that define the tiled scan kernel and its launch configuration, and
+# those of the convolution kernel (its launch lives in mbscan.hip's conv_fwd_k).
 KERNEL_SOURCES = ("scan_tiled.hpp", "device_math.hpp", "scan_params.hpp")
+CONV_KERNEL_SOURCES = ("conv1d.hpp", "device_math.hpp")
 
 
-def kernel_sources_digest() -> str:
+def kernel_sources_digest(sources=KERNEL_SOURCES) -> str:
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in sources:
         with open(os.path.join(_PKG, "csrc", name), "rb") as f:
             h.update(name.encode() + f.read())
     return h.hexdigest()[:16]
@@ -94,7 +96,7 @@ def traffic_record(args) -> dict:
     wr = write * 1024.0 * wfac
     return {
         "kernel": args.kernel,
-        "kernel_sources": kernel_sources_digest(),
+        "kernel_sources": kernel_sources_digest(CONV_KERNEL_SOURCES if args.conv else KERNEL_SOURCES),
         "fetch_size_kib_per_dispatch": round(fetch, 1),
         "write_size_kib_per_dispatch": round(write, 1),
         "copy_calibration": {"bytes": nbytes, "fetch_size_kib": round(cfetch, 1),
@@ -124,6 +126,7 @@ def main(argv=None):
     f.add_argument("--copy-mib", type=int, required=True)
     f.add_argument("--command", dest="commands", action="append", help="command that made a pass")
     f.add_argument("--out", default=TRAFFIC_FILE)
+    f.add_argument("--conv", action="store_true", help="the record is for the convolution kernel")
     args = ap.parse_args(argv)
     if args.cmd == "trace":
         print(json.dumps(trace_table(args.db, args.last), indent=1))

@@ -30,15 +30,15 @@ def declared_functions():
 def test_exports_every_declared_symbol():
     lib = mb.load_library()
     names = declared_functions()
-    assert {"mb_scan_fwd", "mb_scan_fwd_states", "mb_scan_step", "mb_status_string",
-            "mb_abi_version"} <= set(names)
+    assert {"mb_scan_fwd", "mb_scan_fwd_states", "mb_scan_step", "mb_conv1d_fwd", "mb_conv1d_step",
+            "mb_status_string", "mb_abi_version"} <= set(names)
     for n in names:
         assert hasattr(lib, n), f"{n} declared in mbscan.h but not exported"
 
 
 def test_version_and_status_strings():
     lib = mb.load_library()
-    assert lib.mb_abi_version() == 2
+    assert lib.mb_abi_version() == 3
     for code in range(-7, 1):
         assert lib.mb_status_string(code)
     assert lib.mb_status_string(-99) == b"unknown status"
@@ -116,6 +116,64 @@ def _fwd_states(desc, npos, **over):
 ])
 def test_fwd_states_rejects(npos, over, code):
     assert _fwd_states(_desc(), npos, **over) == code
+
+
+def _cdesc(**kw):
+    d = dict(batch=2, dim=8, seqlen=16, width=4, in_dtype=1, out_dtype=1, apply_silu=1, reserved=0,
+             reserved2=0)
+    d.update(kw)
+    return B.ConvDesc(**d)
+
+
+CP = {k: 0x20000000 * (i + 1) for i, k in enumerate(["x", "w", "bias", "sin", "y", "sout"])}
+
+
+def _conv(desc, **over):
+    a = dict(CP)
+    a.update(over)
+    lib = mb.load_library()
+    return lib.mb_conv1d_fwd(ctypes.byref(desc) if desc is not None else None, a["x"], a["w"], a["bias"],
+                             a["sin"], a["y"], a["sout"], None)
+
+
+@no_gpu_only
+@pytest.mark.parametrize("desc,over,code", [
+    (None, {}, -1),
+    (_cdesc(seqlen=-1), {}, -2),
+    (_cdesc(batch=1 << 40, dim=1 << 20, seqlen=1 << 10), {}, -2),
+    (_cdesc(in_dtype=5), {}, -3),
+    (_cdesc(width=0), {}, -5),
+    (_cdesc(width=5), {}, -5),
+    (_cdesc(reserved=1), {}, -5),
+    (_cdesc(reserved2=3), {}, -5),
+    (_cdesc(), dict(x=None), -1),
+    (_cdesc(), dict(w=None), -1),
+    (_cdesc(), dict(y=None), -1),
+    (_cdesc(), dict(x=CP["x"] + 1), -4),
+    (_cdesc(), dict(sout=CP["sout"] + 2), -4),
+    (_cdesc(), dict(y=CP["x"] + 32), -7),                # y inside x
+    (_cdesc(), dict(sout=CP["sin"]), -7),                # state_out on top of state_in
+    (_cdesc(), dict(sout=CP["y"] + 16), -7),             # state_out inside y
+])
+def test_conv_rejects(desc, over, code):
+    assert _conv(desc, **over) == code
+
+
+@no_gpu_only
+def test_conv_step_rejects():
+    lib = mb.load_library()
+    f = lib.mb_conv1d_step
+    ok = [CP["x"], CP["w"], CP["bias"], CP["sin"], CP["y"], None]
+    assert f(-1, 8, 4, 1, 1, 1, *ok) == -2
+    assert f(2, 8, 9, 1, 1, 1, *ok) == -5
+    assert f(2, 8, 4, 2, 1, 1, *ok) == -3
+    bad = list(ok); bad[3] = None                       # the state is required for k > 1
+    assert f(2, 8, 4, 1, 1, 1, *bad) == -1
+    bad = list(ok); bad[4] = CP["x"]                    # y_t on top of x_t
+    assert f(2, 8, 4, 1, 1, 1, *bad) == -7
+    bad = list(ok); bad[3] = CP["w"]                    # state on top of w
+    assert f(2, 8, 4, 1, 1, 1, *bad) == -7
+    assert f(0, 8, 4, 1, 1, 1, *ok) == 0
 
 
 @no_gpu_only
