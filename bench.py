@@ -187,6 +187,65 @@ def bench_conv(args):
     print(json.dumps(line))
 
 
+def bench_rank(args):
+    """One mb_verify_rank per step: the top-3 check (Table 6) of 16 drafted bytes per
+    prompt over fp32 256-way byte logits, batch 32 (the verify workload)."""
+    import torch
+
+    import paper_2401_13660_amd as mb
+
+    B, n, V, beta = 32, 16, 256, 3
+    rng = np.random.default_rng(0)
+    lg = rng.standard_normal((B, n, V)).astype(np.float32)
+    order = np.argsort(-lg.astype(np.float64), axis=2, kind="stable")
+    pick = np.minimum(rng.geometric(0.5, (B, n)) - 1, V - 1)
+    draft = np.take_along_axis(order, pick[..., None], axis=2)[..., 0].astype(np.int32)
+    dev = torch.device("cuda:0")
+    lg_d, dr_d = torch.from_numpy(lg).to(dev), torch.from_numpy(draft).to(dev)
+
+    def step():
+        return mb.verify_rank(lg_d, dr_d, beta, return_ranks=True)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        acc, last, ranks = step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    nbytes = lg.nbytes + draft.nbytes + draft.nbytes + 2 * B * 4
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    line = {
+        "metric": "top-beta verify check: drafted bytes checked per second (batch 32, 16 bytes, 256-way)",
+        "value": round(B * n / (ms * 1e-3), 1), "unit": "bytes/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "verify_rank_b32_n16_v256", "mode": "rank", "batch": B, "ndraft": n,
+                   "vocab": V, "beta": beta, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "algorithmic_bytes": nbytes,
+                     "note": "0.5 MB per call: launch- and latency-bound, not bandwidth-bound"},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import verify_rank as VR
+        t0 = time.perf_counter()
+        r_ref = VR.ranks(lg, draft)
+        a_ref = VR.accepted(r_ref, beta)
+        elapsed = time.perf_counter() - t0
+        ok = np.array_equal(ranks.cpu().numpy(), r_ref) and np.array_equal(acc.cpu().numpy(), a_ref)
+        line["cpu_baseline"] = {"value": round(B * n / elapsed, 1), "unit": "bytes/s", "cores": 1,
+                                "kind": "oracle", "sample": f"the whole check, numpy, {elapsed * 1e3:.1f} ms"}
+        line["parity"] = {"ranks_and_accepted_equal": bool(ok), "ok": bool(ok)}
+        if not ok:
+            print(json.dumps(line))
+            print("parity gate failed: GPU output disagrees with the oracle", file=sys.stderr)
+            sys.exit(1)
+    print(json.dumps(line))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -194,10 +253,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["fwd", "step", "conv"], default="fwd",
+    ap.add_argument("--mode", choices=["fwd", "step", "conv", "rank"], default="fwd",
                     help="fwd: one mb_scan_fwd per step; step: seqlen successive mb_scan_step calls per step "
                          "(the recurrent-generation form of the same workload); conv: one mb_conv1d_fwd "
-                         "(the causal convolution + Swish in front of the scan, k = 4, bf16 out)")
+                         "(the causal convolution + Swish in front of the scan, k = 4, bf16 out); rank: one "
+                         "mb_verify_rank (top-3 check of 16 drafted bytes over 256-way logits, batch 32)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the scan, run a plain device copy of MIB MiB (reference for HBM counters)")
     args = ap.parse_args()
@@ -224,6 +284,8 @@ def main():
 
     if args.mode == "conv":
         return bench_conv(args)
+    if args.mode == "rank":
+        return bench_rank(args)
 
     inp = workload(args.workload, seed=0)
     dev = torch.device("cuda:0")

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define MB_ABI_VERSION 3
+#define MB_ABI_VERSION 4
 
 typedef enum {
     MB_F32 = 0,
@@ -217,6 +217,35 @@ int mb_conv1d_fwd(const mb_conv_desc *desc, const void *x, const float *w, const
 int mb_conv1d_step(int64_t batch, int64_t dim, int32_t width, int32_t in_dtype, int32_t out_dtype,
                    int32_t apply_silu, const void *x_t, const float *w, const float *bias,
                    float *state, void *y_t, void *stream);
+
+/*
+ * The top-beta check that ends a speculative verification (Section 3,
+ * "Speculative decoding through subword drafting"; Appendix F, Algorithm 1;
+ * beta = 3 in Table 6).  For drafted byte i of batch element b:
+ *
+ *   rank   = 1 + the number of candidates y with logits[b][i][y] > logits[b][i][x],
+ *            x = draft[b][i]; vocab + 1 when x is outside [0, vocab) or its logit
+ *            is NaN (such a byte is always rejected).  Ties do not count against x.
+ *            Logits rank exactly like probabilities (a softmax is monotone).
+ *   accepted[b] = the number of leading drafted bytes whose rank is <= beta, i.e.
+ *            the bifurcation position c: bytes 1..c verified, byte c+1 not.
+ *   last_pos[b] = accepted[b] - 1, the 0-based timestep of the last accepted byte
+ *            in the verified chunk (-1: none), which can be passed on device, as
+ *            pos, to mb_scan_fwd_states to recover the state there.
+ *
+ *   logits    act   (batch, ndraft, vocab)  next-byte scores; logits[b][i] scores
+ *                                            drafted byte i
+ *   draft     int32 (batch, ndraft)          the drafted bytes
+ *   beta      any int32 (<= 0 accepts nothing)
+ *   ranks     int32 (batch, ndraft)          output; NULL means not written
+ *   accepted  int32 (batch)                  output; required
+ *   last_pos  int32 (batch)                  output; NULL means not written
+ * Outputs must not overlap each other or the inputs.  vocab >= 1, ndraft and
+ * vocab below 2^31.
+ */
+int mb_verify_rank(int64_t batch, int64_t ndraft, int64_t vocab, int32_t logit_dtype, int32_t beta,
+                   const void *logits, const int32_t *draft, int32_t *ranks, int32_t *accepted,
+                   int32_t *last_pos, void *stream);
 
 /* Static, NUL-terminated description of a status code (never NULL). */
 const char *mb_status_string(int status);

@@ -59,6 +59,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mb_conv1d_fwd.argtypes = [ctypes.POINTER(ConvDesc)] + [_VP] * 7
     lib.mb_conv1d_step.restype = ctypes.c_int
     lib.mb_conv1d_step.argtypes = [ctypes.c_int64] * 2 + [ctypes.c_int32] * 4 + [_VP] * 6
+    lib.mb_verify_rank.restype = ctypes.c_int
+    lib.mb_verify_rank.argtypes = [ctypes.c_int64] * 3 + [ctypes.c_int32] * 2 + [_VP] * 6
     lib.mb_status_string.restype = ctypes.c_char_p
     lib.mb_status_string.argtypes = [ctypes.c_int]
     lib.mb_abi_version.restype = ctypes.c_int
@@ -272,3 +274,25 @@ def conv1d_step(state, x_t, w, bias=None, *, apply_silu=True, out_dtype=None, ou
                                 _ptr(out), stream)
     _check(st, "mb_conv1d_step")
     return out
+
+
+def verify_rank(logits, draft, beta, *, return_ranks=False):
+    """Top-beta check of drafted bytes.  logits: (batch, ndraft, vocab) fp32 or bf16;
+    draft: int32 (batch, ndraft).  Returns (accepted, last_pos), each int32 (batch,),
+    and the int32 (batch, ndraft) ranks when ``return_ranks``."""
+    lib = load_library()
+    if not isinstance(logits, torch.Tensor) or logits.dim() != 3:
+        raise MBScanError("logits must be a (batch, ndraft, vocab) tensor")
+    nb, n, V = logits.shape
+    dev = logits.device
+    _need(logits, "logits", (nb, n, V), None, dev)
+    _need(draft, "draft", (nb, n), torch.int32, dev)
+    accepted = torch.empty(nb, dtype=torch.int32, device=dev)
+    last_pos = torch.empty(nb, dtype=torch.int32, device=dev)
+    ranks = torch.empty((nb, n), dtype=torch.int32, device=dev) if return_ranks else None
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    with torch.cuda.device(dev):
+        st = lib.mb_verify_rank(nb, n, V, _dt(logits.dtype), int(beta), _ptr(logits), _ptr(draft),
+                                _ptr(ranks), _ptr(accepted), _ptr(last_pos), stream)
+    _check(st, "mb_verify_rank")
+    return (accepted, last_pos, ranks) if return_ranks else (accepted, last_pos)

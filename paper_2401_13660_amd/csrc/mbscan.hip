@@ -12,6 +12,7 @@
 #include "scan_rowwise.hpp"
 #include "scan_step.hpp"
 #include "scan_tiled.hpp"
+#include "verify_rank.hpp"
 
 namespace {
 
@@ -342,6 +343,40 @@ int mb_conv1d_step(int64_t batch, int64_t dim, int32_t width, int32_t in_dtype, 
     p.x = x_t; p.w = w; p.bias = bias; p.state_in = state; p.y = y_t; p.state_out = state;
     p.apply_silu = apply_silu ? 1 : 0;
     const hipError_t e = conv_launch(p, in_dtype, out_dtype, width, true, false, stream);
+    return e == hipSuccess ? MB_OK : MB_ERR_HIP;
+}
+
+int mb_verify_rank(int64_t batch, int64_t ndraft, int64_t vocab, int32_t logit_dtype, int32_t beta,
+                   const void *logits, const int32_t *draft, int32_t *ranks, int32_t *accepted,
+                   int32_t *last_pos, void *stream) {
+    if (batch < 0 || ndraft < 0 || vocab < 1) return MB_ERR_SHAPE;
+    if (ndraft >= (int64_t(1) << 31) || vocab >= (int64_t(1) << 31) - 1 || batch >= (int64_t(1) << 31))
+        return MB_ERR_SHAPE;
+    if (!valid_dtype(logit_dtype)) return MB_ERR_DTYPE;
+    int64_t pairs, elems;
+    if (!mul_ok(batch, ndraft, &pairs) || !mul_ok(pairs, vocab, &elems)) return MB_ERR_SHAPE;
+    if (batch == 0) return MB_OK;
+    if (!accepted || (ndraft > 0 && (!logits || !draft))) return MB_ERR_NULL;
+    const size_t lsz = dtype_size(logit_dtype);
+    if ((logits && !aligned(logits, lsz)) || (draft && !aligned(draft, 4)) || !aligned(accepted, 4) ||
+        (ranks && !aligned(ranks, 4)) || (last_pos && !aligned(last_pos, 4)))
+        return MB_ERR_ALIGN;
+    const size_t l_bytes = (size_t)elems * lsz, d_bytes = (size_t)pairs * 4, b_bytes = (size_t)batch * 4;
+    struct Range { const void *p; size_t n; } outs[] = {{ranks, d_bytes}, {accepted, b_bytes}, {last_pos, b_bytes}};
+    for (int i = 0; i < 3; ++i) {
+        if (overlaps(outs[i].p, outs[i].n, logits, l_bytes) || overlaps(outs[i].p, outs[i].n, draft, d_bytes))
+            return MB_ERR_ALIAS;
+        for (int j = i + 1; j < 3; ++j)
+            if (overlaps(outs[i].p, outs[i].n, outs[j].p, outs[j].n)) return MB_ERR_ALIAS;
+    }
+    mbs::rank::RankParams p{};
+    p.batch = batch; p.ndraft = ndraft; p.vocab = vocab; p.logits = logits; p.draft = draft; p.beta = beta;
+    p.ranks = ranks; p.accepted = accepted; p.last_pos = last_pos;
+    const void *fn = logit_dtype == MB_F32 ? reinterpret_cast<const void *>(&mbs::rank::verify_rank<0>)
+                                           : reinterpret_cast<const void *>(&mbs::rank::verify_rank<1>);
+    const int waves = ndraft < 1 ? 1 : (ndraft > mbs::rank::kMaxThreads / 64 ? mbs::rank::kMaxThreads / 64
+                                                                               : (int)ndraft);
+    const hipError_t e = launch(fn, dim3((unsigned)batch), dim3(64 * waves), &p, stream);
     return e == hipSuccess ? MB_OK : MB_ERR_HIP;
 }
 

@@ -31,14 +31,14 @@ def test_exports_every_declared_symbol():
     lib = mb.load_library()
     names = declared_functions()
     assert {"mb_scan_fwd", "mb_scan_fwd_states", "mb_scan_step", "mb_conv1d_fwd", "mb_conv1d_step",
-            "mb_status_string", "mb_abi_version"} <= set(names)
+            "mb_verify_rank", "mb_status_string", "mb_abi_version"} <= set(names)
     for n in names:
         assert hasattr(lib, n), f"{n} declared in mbscan.h but not exported"
 
 
 def test_version_and_status_strings():
     lib = mb.load_library()
-    assert lib.mb_abi_version() == 3
+    assert lib.mb_abi_version() == 4
     for code in range(-7, 1):
         assert lib.mb_status_string(code)
     assert lib.mb_status_string(-99) == b"unknown status"
@@ -174,6 +174,33 @@ def test_conv_step_rejects():
     bad = list(ok); bad[3] = CP["w"]                    # state on top of w
     assert f(2, 8, 4, 1, 1, 1, *bad) == -7
     assert f(0, 8, 4, 1, 1, 1, *ok) == 0
+
+
+RP = {k: 0x30000000 * (i + 1) for i, k in enumerate(["logits", "draft", "ranks", "acc", "last"])}
+
+
+@no_gpu_only
+@pytest.mark.parametrize("args,over,code", [
+    ((-1, 16, 256), {}, -2),
+    ((4, -1, 256), {}, -2),
+    ((4, 16, 0), {}, -2),
+    ((4, 1 << 31, 256), {}, -2),
+    ((4, 16, 256, 7), {}, -3),
+    ((4, 16, 256), dict(acc=None), -1),
+    ((4, 16, 256), dict(logits=None), -1),
+    ((4, 16, 256), dict(draft=RP["draft"] + 2), -4),
+    ((4, 16, 256), dict(acc=RP["logits"] + 64), -7),     # output inside the logits
+    ((4, 16, 256), dict(last=RP["acc"]), -7),            # two outputs on top of each other
+    ((4, 16, 256), dict(ranks=RP["draft"]), -7),
+])
+def test_verify_rank_rejects(args, over, code):
+    a = dict(RP)
+    a.update(over)
+    batch, n, V = args[:3]
+    dt = args[3] if len(args) > 3 else 0
+    lib = mb.load_library()
+    assert lib.mb_verify_rank(batch, n, V, dt, 3, a["logits"], a["draft"], a["ranks"], a["acc"], a["last"],
+                              None) == code
 
 
 @no_gpu_only
