@@ -63,6 +63,11 @@ class Oracle:
             ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
             _D, _D, _D, _D, _D, _D, _D, _I64, ctypes.c_int64, _D, _D, _D, _D,
             _I64, ctypes.c_int64, _D]
+        self.lib.mbo_scan_bwd_rows.restype = ctypes.c_int
+        self.lib.mbo_scan_bwd_rows.argtypes = [
+            ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+            _D, _D, _D, _D, _D, _D, _D, _I64, ctypes.c_int64, _D, _D, _D, _D,
+            _D, _D, _D, _D, _D, _D, _D, _D, _D]
         self.lib.mbo_conv1d_rows.restype = ctypes.c_int
         self.lib.mbo_conv1d_rows.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
                                              _D, _D, _D, _D, _D, _D]
@@ -193,6 +198,57 @@ class Oracle:
             raise ValueError(f"oracle rejected the arguments (status {rc})")
         return y.reshape(nb, dim), h_new
 
+
+    # -- the backward of the scan -------------------------------------------------
+    def scan_bwd(self, u, delta, A, Bm, Cm, dy, *, z=None, Dskip=None, dt_bias=None, h0=None,
+                 dh_last=None, delta_softplus=True, dtype: str | None = None):
+        """Gradients of sum(dy * y) + sum(dh_last * h_last) for (batch, dim, L) inputs.
+
+        Activations may be bf16 bit patterns (``dtype="bf16"``).  Returns a dict of fp64
+        arrays: du, ddelta, dz (batch, dim, L); dA (dim, N); dB, dC (batch, N, L);
+        dD, dbias (dim,); dh0 (batch, dim, N).  Absent inputs get no gradient (None).
+        """
+        u = np.asarray(u)
+        nb, dim, L = u.shape
+        N = np.asarray(A).shape[1]
+        R = nb * dim
+        bidx = np.repeat(np.arange(nb, dtype=np.int64), dim)
+        didx = np.tile(np.arange(dim), nb)
+
+        def act(x):
+            return None if x is None else np.ascontiguousarray(to_f64(x, dtype).reshape(R, L))
+
+        def flat(x, width):
+            return None if x is None else np.ascontiguousarray(to_f64(x).reshape(R, width))
+
+        Af = np.ascontiguousarray(to_f64(A)[didx])
+        Ds = None if Dskip is None else np.ascontiguousarray(to_f64(Dskip)[didx])
+        db = None if dt_bias is None else np.ascontiguousarray(to_f64(dt_bias)[didx])
+        Bf = np.ascontiguousarray(to_f64(Bm, dtype))
+        Cf = np.ascontiguousarray(to_f64(Cm, dtype))
+        zf = act(z)
+        out = {k: np.empty((R, L)) for k in ("du", "ddelta")}
+        out["dz"] = np.empty((R, L)) if z is not None else None
+        dA = np.empty((R, N))
+        dD = np.empty(R)
+        dbias = np.empty(R)
+        dh0 = np.empty((R, N))
+        dB = np.empty((nb, N, L))
+        dC = np.empty((nb, N, L))
+        rc = self.lib.mbo_scan_bwd_rows(
+            R, L, N, int(bool(delta_softplus)), _ptr(act(u)), _ptr(act(delta)), _ptr(zf), _ptr(Af),
+            _ptr(Ds), _ptr(db), _ptr(flat(h0, N)), bidx.ctypes.data_as(_I64), nb, _ptr(Bf), _ptr(Cf),
+            _ptr(act(dy)), _ptr(flat(dh_last, N)), _ptr(out["du"]), _ptr(out["ddelta"]), _ptr(out["dz"]),
+            _ptr(dA), _ptr(dD), _ptr(dbias), _ptr(dh0), _ptr(dB), _ptr(dC))
+        if rc != 0:
+            raise ValueError(f"oracle rejected the arguments (status {rc})")
+        g = {k: (None if v is None else v.reshape(nb, dim, L)) for k, v in out.items()}
+        g["dA"] = dA.reshape(nb, dim, N).sum(axis=0)
+        g["dD"] = dD.reshape(nb, dim).sum(axis=0) if Dskip is not None else None
+        g["dbias"] = dbias.reshape(nb, dim).sum(axis=0) if dt_bias is not None else None
+        g["dh0"] = dh0.reshape(nb, dim, N)
+        g["dB"], g["dC"] = dB, dC
+        return g
 
     # -- the causal depthwise convolution ---------------------------------------
     def conv1d(self, x, w, *, bias=None, state=None, apply_silu=True, dtype: str | None = None):

@@ -47,6 +47,22 @@
  *   y[r][t]  = silu(pre[t]) if apply_silu else pre[t]
  *   state_out[r][j] = xin(L - (k-1) + j)   for j < k - 1
  *
+ * And the backward of the scan (training at the 8,192-byte context, Section 4,
+ * Appendix C): given dy (and optionally dh_last), the gradients with respect to
+ * every input, by reverse-mode differentiation of the loop above.  With
+ * lambda_t[n] the total gradient of the loss with respect to h_t[n]:
+ *
+ *   ds_t        = dy_t * silu(z_t)  (dy_t without a gate)
+ *   dz_t        = dy_t * s_t * silu'(z_t),  s_t = sum_n C_t[n] h_t[n] + Dskip u_t
+ *   lambda_t[n] = ds_t C_t[n] + abar_{t+1}[n] lambda_{t+1}[n]   (+ dh_last at t = L-1)
+ *   dC_t[n]    += ds_t h_t[n]                    (summed over the channels of a batch element)
+ *   dB_t[n]    += lambda_t[n] dlt_t u_t          (idem)
+ *   du_t        = ds_t Dskip + sum_n lambda_t[n] dlt_t B_t[n]
+ *   ddlt_t      = sum_n lambda_t[n] (A[n] abar_t[n] h_{t-1}[n] + B_t[n] u_t)
+ *   ddelta_t    = ddlt_t * sigmoid(v_t) with softplus, ddlt_t without; dbias += ddelta_t
+ *   dA[n]      += lambda_t[n] dlt_t abar_t[n] h_{t-1}[n];  dDskip += ds_t u_t
+ *   dh0[n]      = abar_0[n] lambda_0[n]
+ *
  * Parity pinned by tests/test_oracle_pins.py (brute-force materialisation on
  * the time grid t_k = sum Delta, geometric closed form, B = 0, split
  * invariance, the eq. (4) gated-recurrence special case, the associative
@@ -219,6 +235,130 @@ int mbo_scan_step(int64_t R, int64_t N, int delta_softplus,
         scan_one_row(r, 1, N, delta_softplus, u_t, delta_t, z_t, A, Dskip, dt_bias,
                      h, bidx, B_t, C_t, y_t, h, NULL, 0, NULL);
     }
+    return MBO_OK;
+}
+
+/* ---- the backward of the scan ---------------------------------------------- */
+
+static double sigmoid(double v)
+{
+    return 1.0 / (1.0 + exp(-v));
+}
+
+/* Per-row outputs (du, ddelta, dz, dA_row, dD_row, dbias_row, dh0) are written;
+ * dB and dC (nbatch x N x L) are accumulated over rows. */
+static void bwd_one_row(int64_t r, int64_t L, int64_t N, int delta_softplus,
+                        const double *u, const double *delta, const double *z,
+                        const double *A, const double *Dskip, const double *dt_bias,
+                        const double *h0, const int64_t *bidx,
+                        const double *Bm, const double *Cm,
+                        const double *dy, const double *dh_last,
+                        double *du, double *ddelta, double *dz, double *dA, double *dD,
+                        double *dbias, double *dh0, double *dB, double *dC)
+{
+    const int64_t b = bidx[r];
+    /* forward, keeping every state (hs[t + 1] = h_t, hs[0] = h_{-1}) */
+    double *hs = malloc(sizeof(double) * (size_t)(L + 1) * (size_t)N);
+    double *dl = malloc(sizeof(double) * (size_t)(L > 0 ? L : 1));
+    double *sv = malloc(sizeof(double) * (size_t)(L > 0 ? L : 1));
+    for (int64_t n = 0; n < N; ++n)
+        hs[n] = h0 ? h0[r * N + n] : 0.0;
+    for (int64_t t = 0; t < L; ++t) {
+        const double x = u[r * L + t];
+        const double v = delta[r * L + t] + (dt_bias ? dt_bias[r] : 0.0);
+        dl[t] = delta_softplus ? softplus(v) : v;
+        double acc = Dskip ? Dskip[r] * x : 0.0;
+        for (int64_t n = 0; n < N; ++n) {
+            const double ab = exp(dl[t] * A[r * N + n]);
+            hs[(t + 1) * N + n] = ab * hs[t * N + n] + (dl[t] * Bm[(b * N + n) * L + t]) * x;
+            acc += Cm[(b * N + n) * L + t] * hs[(t + 1) * N + n];
+        }
+        sv[t] = acc;
+    }
+    /* reverse */
+    double lam_next[MBO_MAX_N];      /* abar_{t+1} lambda_{t+1}: the gradient reaching h_t through h_{t+1} */
+    for (int64_t n = 0; n < N; ++n) {
+        lam_next[n] = dh_last ? dh_last[r * N + n] : 0.0;
+        dA[r * N + n] = 0.0;
+    }
+    double sum_dD = 0.0, sum_dbias = 0.0;
+    for (int64_t t = L - 1; t >= 0; --t) {
+        const double x = u[r * L + t];
+        const double g = z ? silu(z[r * L + t]) : 1.0;
+        const double ds = dy[r * L + t] * g;
+        if (z) {
+            const double zz = z[r * L + t], sg = sigmoid(zz);
+            dz[r * L + t] = dy[r * L + t] * sv[t] * sg * (1.0 + zz * (1.0 - sg));
+        }
+        sum_dD += ds * x;
+        double dut = ds * (Dskip ? Dskip[r] : 0.0);
+        double ddl = 0.0;
+        for (int64_t n = 0; n < N; ++n) {
+            const double Bv = Bm[(b * N + n) * L + t], Cv = Cm[(b * N + n) * L + t];
+            const double ab = exp(dl[t] * A[r * N + n]);
+            const double hprev = hs[t * N + n], hcur = hs[(t + 1) * N + n];
+            const double lam = ds * Cv + lam_next[n];
+#pragma omp atomic
+            dC[(b * N + n) * L + t] += ds * hcur;
+#pragma omp atomic
+            dB[(b * N + n) * L + t] += lam * dl[t] * x;
+            dut += lam * dl[t] * Bv;
+            ddl += lam * (A[r * N + n] * ab * hprev + Bv * x);
+            dA[r * N + n] += lam * dl[t] * ab * hprev;
+            lam_next[n] = lam * ab;
+        }
+        du[r * L + t] = dut;
+        const double v = delta[r * L + t] + (dt_bias ? dt_bias[r] : 0.0);
+        const double dv = delta_softplus ? ddl * sigmoid(v) : ddl;
+        ddelta[r * L + t] = dv;
+        sum_dbias += dv;
+    }
+    dD[r] = sum_dD;
+    dbias[r] = sum_dbias;
+    if (dh0)
+        for (int64_t n = 0; n < N; ++n)
+            dh0[r * N + n] = lam_next[n];
+    free(hs);
+    free(dl);
+    free(sv);
+}
+
+/*
+ * Backward over R rows.  Inputs as for mbo_scan_rows, plus
+ *   dy        : R x L       gradient of the loss with respect to y
+ *   dh_last   : R x N       gradient with respect to h_last (may be NULL: zero)
+ * Outputs
+ *   du, ddelta: R x L;  dz: R x L (may be NULL when z is NULL)
+ *   dA        : R x N       per row (the caller sums the rows of a channel)
+ *   dD, dbias : R           per row (idem)
+ *   dh0       : R x N       (may be NULL)
+ *   dB, dC    : nbatch x N x L, overwritten with the sums over the rows of each batch element
+ */
+int mbo_scan_bwd_rows(int64_t R, int64_t L, int64_t N, int delta_softplus,
+                      const double *u, const double *delta, const double *z,
+                      const double *A, const double *Dskip, const double *dt_bias,
+                      const double *h0, const int64_t *bidx, int64_t nbatch,
+                      const double *Bm, const double *Cm,
+                      const double *dy, const double *dh_last,
+                      double *du, double *ddelta, double *dz, double *dA, double *dD,
+                      double *dbias, double *dh0, double *dB, double *dC)
+{
+    if (R < 0 || L < 0 || N < 1 || N > MBO_MAX_N || nbatch < 1)
+        return MBO_ERR_ARG;
+    if (!u || !delta || !A || !bidx || !Bm || !Cm || !dy || !du || !ddelta || !dA || !dD || !dbias ||
+        !dB || !dC || (z && !dz))
+        return MBO_ERR_ARG;
+    for (int64_t r = 0; r < R; ++r)
+        if (bidx[r] < 0 || bidx[r] >= nbatch)
+            return MBO_ERR_ARG;
+    for (int64_t i = 0; i < nbatch * N * L; ++i) {
+        dB[i] = 0.0;
+        dC[i] = 0.0;
+    }
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < R; ++r)
+        bwd_one_row(r, L, N, delta_softplus, u, delta, z, A, Dskip, dt_bias, h0, bidx, Bm, Cm,
+                    dy, dh_last, du, ddelta, dz, dA, dD, dbias, dh0, dB, dC);
     return MBO_OK;
 }
 

@@ -334,6 +334,69 @@ def pin_states_at_positions(orc):
                 _close(hp[k, b], ref, 1e-11, f"state at position {p} (seed {seed}, k {k}, b {b})")
 
 
+# ---- the backward of the scan: reverse-mode gradients against central finite
+#      differences of the (pinned) forward -----------------------------------
+
+_GRAD_OF = dict(u="du", delta="ddelta", z="dz", A="dA", B="dB", C="dC", Dskip="dD", dt_bias="dbias",
+                h0="dh0")
+
+
+def _bwd_loss(orc, c, dy, dhl, delta_softplus):
+    y, h = _run(orc, c, delta_softplus=delta_softplus)
+    return float(np.sum(dy * y) + (0.0 if dhl is None else np.sum(dhl * h)))
+
+
+def _bwd_grads(orc, c, dy, dhl, delta_softplus):
+    return orc.scan_bwd(c["u"], c["delta"], c["A"], c["B"], c["C"], dy, z=c["z"], Dskip=c["Dskip"],
+                        dt_bias=c["dt_bias"], h0=c["h0"], dh_last=dhl, delta_softplus=delta_softplus)
+
+
+def pin_bwd_finite_differences(orc):
+    """Every gradient agrees with a central difference of the forward oracle's loss
+    sum(dy y) + sum(dh_last h_last) at sampled elements."""
+    cases = ((51, {}, True, True), (52, dict(gated=False, h0=False), True, False),
+             (53, dict(D=False, bias=False), False, True))
+    for seed, kw, sp, with_dhl in cases:
+        c = _rand_case(seed, nb=2, dim=3, L=11, N=4, **kw)
+        if not sp:                               # keep Delta positive without softplus
+            c["delta"] = np.abs(c["delta"]) * 0.2 + 0.01
+        rng = np.random.default_rng(seed + 100)
+        dy = rng.standard_normal(c["u"].shape)
+        dhl = rng.standard_normal((2, 3, 4)) if with_dhl else None
+        g = _bwd_grads(orc, c, dy, dhl, sp)
+        for name, gname in _GRAD_OF.items():
+            if c[name] is None:
+                continue
+            x = c[name]
+            for _ in range(4):
+                idx = tuple(int(rng.integers(0, n)) for n in x.shape)
+                eps = 1e-6 * max(1.0, abs(x[idx]))
+                old = x[idx]
+                x[idx] = old + eps
+                lp = _bwd_loss(orc, c, dy, dhl, sp)
+                x[idx] = old - eps
+                lm = _bwd_loss(orc, c, dy, dhl, sp)
+                x[idx] = old
+                fd = (lp - lm) / (2 * eps)
+                an = g[gname][idx]
+                assert abs(fd - an) <= 1e-6 * (abs(fd) + 1.0), \
+                    f"{gname}{idx} seed {seed}: analytic {an:.9g} vs finite difference {fd:.9g}"
+
+
+def pin_bwd_linearity(orc):
+    """Gradients are linear in the incoming (dy, dh_last)."""
+    c = _rand_case(54, nb=2, dim=2, L=9, N=3)
+    rng = np.random.default_rng(55)
+    d1, d2 = rng.standard_normal(c["u"].shape), rng.standard_normal(c["u"].shape)
+    h1, h2 = rng.standard_normal((2, 2, 3)), rng.standard_normal((2, 2, 3))
+    g1 = _bwd_grads(orc, c, d1, h1, True)
+    g2 = _bwd_grads(orc, c, d2, h2, True)
+    g12 = _bwd_grads(orc, c, 2.0 * d1 - d2, 2.0 * h1 - h2, True)
+    for k, v in g12.items():
+        if v is not None:
+            _close(v, 2.0 * g1[k] - g2[k], 1e-12, f"bwd linearity {k}")
+
+
 # ---- the causal depthwise convolution upstream of the scan (Table 8, "Pre-SSM
 #      1D convolution"; Fig. 5, right: Swish after the convolution) -----------
 
@@ -409,4 +472,5 @@ ALL_PINS = [
     pin_tuple_scan, pin_separability, pin_linearity, pin_step_equals_fwd, pin_limits,
     pin_softplus_extremes, pin_states_at_positions,
     pin_conv_library, pin_conv_impulse, pin_conv_split_and_step,
+    pin_bwd_finite_differences, pin_bwd_linearity,
 ]

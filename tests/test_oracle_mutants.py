@@ -59,6 +59,18 @@ MUTANTS = [
      "state_out[r * H + j] = src >= 0 ? x[r * L + (src > 0 ? src - 1 : 0)]"),
     ("conv_no_silu", "y[r * L + t] = apply_silu ? silu(pre) : pre;", "y[r * L + t] = pre;"),
     ("conv_silu_always", "y[r * L + t] = apply_silu ? silu(pre) : pre;", "y[r * L + t] = silu(pre);"),
+    ("bwd_carry_without_abar", "lam_next[n] = lam * ab;", "lam_next[n] = lam;"),
+    ("bwd_dC_uses_previous_state", "dC[(b * N + n) * L + t] += ds * hcur;", "dC[(b * N + n) * L + t] += ds * hprev;"),
+    ("bwd_dB_missing_x", "dB[(b * N + n) * L + t] += lam * dl[t] * x;", "dB[(b * N + n) * L + t] += lam * dl[t];"),
+    ("bwd_ddelta_missing_Bx", "ddl += lam * (A[r * N + n] * ab * hprev + Bv * x);",
+     "ddl += lam * (A[r * N + n] * ab * hprev);"),
+    ("bwd_dA_uses_current_state", "dA[r * N + n] += lam * dl[t] * ab * hprev;",
+     "dA[r * N + n] += lam * dl[t] * ab * hcur;"),
+    ("bwd_dz_sigmoid_only", "sg * (1.0 + zz * (1.0 - sg))", "sg"),
+    ("bwd_dh_last_ignored", "lam_next[n] = dh_last ? dh_last[r * N + n] : 0.0;", "lam_next[n] = 0.0;"),
+    ("bwd_softplus_grad_dropped", "ddl * sigmoid(v)", "ddl"),
+    ("bwd_ds_without_gate", "const double ds = dy[r * L + t] * g;", "const double ds = dy[r * L + t];"),
+    ("bwd_du_without_skip", "double dut = ds * (Dskip ? Dskip[r] : 0.0);", "double dut = 0.0;"),
     ("last_state_dropped_from_y", "for (int64_t n = 0; n < N; ++n) {\n            const double abar",
      "for (int64_t n = 0; n < N; ++n) {\n            if (n == N - 1 && N > 1) continue;\n            const double abar"),
 ]
