@@ -187,6 +187,99 @@ def bench_conv(args):
     print(json.dumps(line))
 
 
+def bwd_bytes(inp) -> int:
+    """Each input read once and each output written once: u, delta, z, dy in and du,
+    ddelta, dz out (bf16), B and C in (bf16), dB and dC out (fp32), the parameters."""
+    E = inp.batch * inp.dim * inp.seqlen
+    bnl = inp.batch * inp.dstate * inp.seqlen
+    b = E * 2 * (4 + 3) + bnl * (2 * 2 + 2 * 4)
+    b += inp.dim * inp.dstate * 4 * 2 + inp.dim * 4 * 2 * 2
+    b += inp.batch * inp.dim * inp.dstate * 4 * (1 + (inp.h0 is not None))
+    return int(b)
+
+
+def bench_bwd(args):
+    """One mb_scan_bwd per step over the workload: the backward of the scan in the
+    training setting (bf16 activations and incoming gradient, bf16 activation
+    gradients, fp32 parameter gradients)."""
+    import torch
+
+    import paper_2401_13660_amd as mb
+    from paper_2401_13660_amd.inputs import WORKLOADS, workload
+
+    inp = workload(args.workload, seed=0)
+    dev = torch.device("cuda:0")
+
+    def t(a):
+        if a is None:
+            return None
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    g = {k: t(v) for k, v in inp.arrays().items()}
+    dy = torch.randn(inp.u.shape, generator=torch.Generator().manual_seed(1)).to(dev).to(torch.bfloat16)
+
+    def step():
+        return mb.scan_bwd(g["u"], g["delta"], g["A"], g["B"], g["C"], dy, D=g.get("Dskip"),
+                           dt_bias=g.get("dt_bias"), z=g.get("z"), h0=g.get("h0"))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        grads = step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    E = inp.batch * inp.dim * inp.seqlen
+    nbytes = bwd_bytes(inp)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    line = {
+        "metric": "selective-scan backward: B·L·D elems/s (972M layer, L=8192)",
+        "value": round(E / (ms * 1e-3), 1), "unit": "elems/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": args.workload, "mode": "bwd",
+                   **{k: v for k, v in WORKLOADS[args.workload].items()},
+                   "dy_dtype": "bf16", "grad_dtype": "bf16 (activations), f32 (parameters, dB, dC)",
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None, "algorithmic_bytes": nbytes},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        from parity import rel_err
+
+        orc = oracle.default()
+        import dataclasses
+        nb = 1                                      # a bounded sample: the first batch element
+        cut = lambda a: None if a is None else np.ascontiguousarray(a[:nb])
+        sub = dataclasses.replace(inp, batch=nb, u=cut(inp.u), delta=cut(inp.delta), z=cut(inp.z), B=cut(inp.B),
+                                  C=cut(inp.C), h0=cut(inp.h0))
+        dy_bits = dy[:nb].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        t0 = time.perf_counter()
+        ref = orc.scan_bwd(sub.u, sub.delta, sub.A, sub.B, sub.C, dy_bits, z=sub.z, Dskip=sub.Dskip,
+                           dt_bias=sub.dt_bias, h0=sub.h0, dtype=sub.dtype)
+        elapsed = time.perf_counter() - t0
+        Es = sub.batch * sub.dim * sub.seqlen
+        err = max(rel_err(grads["du"][:nb].float().cpu().numpy(), ref["du"]),
+                  rel_err(grads["dB"][:nb].cpu().numpy(), ref["dB"]))
+        ok = err <= 1e-4 + 2.0 ** -8
+        line["cpu_baseline"] = {"value": round(Es / elapsed, 1), "unit": "elems/s", "cores": orc.max_threads(),
+                                "kind": "oracle",
+                                "sample": f"batch element 0: {sub.dim} rows of L={sub.seqlen}, fp64, {elapsed:.1f} s"}
+        line["parity"] = {"du_dB_rel_err_vs_oracle": err, "ok": bool(ok)}
+        if not ok:
+            print(json.dumps(line))
+            print("parity gate failed: GPU output disagrees with the oracle", file=sys.stderr)
+            sys.exit(1)
+    print(json.dumps(line))
+
+
 def bench_rank(args):
     """One mb_verify_rank per step: the top-3 check (Table 6) of 16 drafted bytes per
     prompt over fp32 256-way byte logits, batch 32 (the verify workload)."""
@@ -253,11 +346,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["fwd", "step", "conv", "rank"], default="fwd",
+    ap.add_argument("--mode", choices=["fwd", "step", "conv", "rank", "bwd"], default="fwd",
                     help="fwd: one mb_scan_fwd per step; step: seqlen successive mb_scan_step calls per step "
                          "(the recurrent-generation form of the same workload); conv: one mb_conv1d_fwd "
                          "(the causal convolution + Swish in front of the scan, k = 4, bf16 out); rank: one "
-                         "mb_verify_rank (top-3 check of 16 drafted bytes over 256-way logits, batch 32)")
+                         "mb_verify_rank (top-3 check of 16 drafted bytes over 256-way logits, batch 32); "
+                         "bwd: one mb_scan_bwd (bf16 dy and activation gradients, fp32 parameter gradients)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the scan, run a plain device copy of MIB MiB (reference for HBM counters)")
     args = ap.parse_args()
@@ -286,6 +380,8 @@ def main():
         return bench_conv(args)
     if args.mode == "rank":
         return bench_rank(args)
+    if args.mode == "bwd":
+        return bench_bwd(args)
 
     inp = workload(args.workload, seed=0)
     dev = torch.device("cuda:0")

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define MB_ABI_VERSION 4
+#define MB_ABI_VERSION 5
 
 typedef enum {
     MB_F32 = 0,
@@ -158,6 +158,36 @@ int mb_scan_step(int64_t batch, int64_t dim, int64_t dstate,
                  const void *B_t, const void *C_t,
                  const float *Dskip, const float *dt_bias, const void *z_t,
                  float *h, void *y_t, void *stream);
+
+/*
+ * The backward of mb_scan_fwd (training at the 8,192-byte context: Section 4,
+ * Appendix C): the gradients of sum(dy * y) + sum(dh_last * h_last) with
+ * respect to every input of the scan, by reverse-mode differentiation of eq. (2)
+ * with the discretisation of Appendix D and Table 8's output and gating.
+ *
+ *   desc, u, delta, A, Bmat, Cmat, Dskip, dt_bias, z, h0   as for mb_scan_fwd
+ *   dy        out-dtype (B, D, L)   gradient with respect to y (desc->out_dtype)
+ *   dh_last   float (B, D, N)       gradient with respect to h_last; NULL means 0
+ *   du, ddelta, dz   out-dtype (B, D, L)   dz is required when z is given
+ *   dA        float (D, N)          summed over batch and time
+ *   dB, dC    float (B, N, L)       summed over the channels of each batch element
+ *   dDskip, ddt_bias float (D)      required when Dskip / dt_bias are given
+ *   dh0       float (B, D, N)       NULL means not written
+ * Outputs are overwritten (not accumulated) and must not overlap any other
+ * argument.  Supported: dstate 16, L a multiple of 16, every activation pointer
+ * 16-byte aligned and every float pointer 8-byte aligned (MB_ERR_UNSUPPORTED /
+ * MB_ERR_ALIGN otherwise).  Results are deterministic.  The call allocates a
+ * stream-ordered workspace (hipMallocAsync): state checkpoints every 16 bytes
+ * (L/16 x B x D x 16 floats) and per-8-channel dB/dC partials (B x L x D/8 x 64
+ * bytes), freed on the same stream.
+ */
+int mb_scan_bwd(const mb_scan_desc *desc,
+                const void *u, const void *delta, const float *A,
+                const void *Bmat, const void *Cmat,
+                const float *Dskip, const float *dt_bias, const void *z,
+                const float *h0, const void *dy, const float *dh_last,
+                void *du, void *ddelta, void *dz, float *dA, float *dB, float *dC,
+                float *dDskip, float *ddt_bias, float *dh0, void *stream);
 
 /*
  * The causal depthwise convolution upstream of the scan.  In the Mamba block

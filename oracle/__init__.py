@@ -204,7 +204,8 @@ class Oracle:
                  dh_last=None, delta_softplus=True, dtype: str | None = None):
         """Gradients of sum(dy * y) + sum(dh_last * h_last) for (batch, dim, L) inputs.
 
-        Activations may be bf16 bit patterns (``dtype="bf16"``).  Returns a dict of fp64
+        Activations may be bf16 bit patterns (``dtype="bf16"``); dy is decoded by its own
+        type (uint16 arrays are bf16 bit patterns).  Returns a dict of fp64
         arrays: du, ddelta, dz (batch, dim, L); dA (dim, N); dB, dC (batch, N, L);
         dD, dbias (dim,); dh0 (batch, dim, N).  Absent inputs get no gradient (None).
         """
@@ -238,7 +239,7 @@ class Oracle:
         rc = self.lib.mbo_scan_bwd_rows(
             R, L, N, int(bool(delta_softplus)), _ptr(act(u)), _ptr(act(delta)), _ptr(zf), _ptr(Af),
             _ptr(Ds), _ptr(db), _ptr(flat(h0, N)), bidx.ctypes.data_as(_I64), nb, _ptr(Bf), _ptr(Cf),
-            _ptr(act(dy)), _ptr(flat(dh_last, N)), _ptr(out["du"]), _ptr(out["ddelta"]), _ptr(out["dz"]),
+            _ptr(np.ascontiguousarray(to_f64(dy).reshape(R, L))), _ptr(flat(dh_last, N)), _ptr(out["du"]), _ptr(out["ddelta"]), _ptr(out["dz"]),
             _ptr(dA), _ptr(dD), _ptr(dbias), _ptr(dh0), _ptr(dB), _ptr(dC))
         if rc != 0:
             raise ValueError(f"oracle rejected the arguments (status {rc})")

@@ -246,7 +246,7 @@ static double sigmoid(double v)
 }
 
 /* Per-row outputs (du, ddelta, dz, dA_row, dD_row, dbias_row, dh0) are written;
- * dB and dC (nbatch x N x L) are accumulated over rows. */
+ * dB and dC (nbatch x N x L) are accumulated into the calling thread's buffers. */
 static void bwd_one_row(int64_t r, int64_t L, int64_t N, int delta_softplus,
                         const double *u, const double *delta, const double *z,
                         const double *A, const double *Dskip, const double *dt_bias,
@@ -298,9 +298,7 @@ static void bwd_one_row(int64_t r, int64_t L, int64_t N, int delta_softplus,
             const double ab = exp(dl[t] * A[r * N + n]);
             const double hprev = hs[t * N + n], hcur = hs[(t + 1) * N + n];
             const double lam = ds * Cv + lam_next[n];
-#pragma omp atomic
             dC[(b * N + n) * L + t] += ds * hcur;
-#pragma omp atomic
             dB[(b * N + n) * L + t] += lam * dl[t] * x;
             dut += lam * dl[t] * Bv;
             ddl += lam * (A[r * N + n] * ab * hprev + Bv * x);
@@ -351,14 +349,28 @@ int mbo_scan_bwd_rows(int64_t R, int64_t L, int64_t N, int delta_softplus,
     for (int64_t r = 0; r < R; ++r)
         if (bidx[r] < 0 || bidx[r] >= nbatch)
             return MBO_ERR_ARG;
-    for (int64_t i = 0; i < nbatch * N * L; ++i) {
+    const int64_t nbc = nbatch * N * L;
+    for (int64_t i = 0; i < nbc; ++i) {
         dB[i] = 0.0;
         dC[i] = 0.0;
     }
-#pragma omp parallel for schedule(dynamic, 1)
-    for (int64_t r = 0; r < R; ++r)
-        bwd_one_row(r, L, N, delta_softplus, u, delta, z, A, Dskip, dt_bias, h0, bidx, Bm, Cm,
-                    dy, dh_last, du, ddelta, dz, dA, dD, dbias, dh0, dB, dC);
+    /* each thread sums its rows' dB / dC into buffers of its own, merged at the end */
+#pragma omp parallel
+    {
+        double *myB = calloc((size_t)(nbc > 0 ? nbc : 1), sizeof(double));
+        double *myC = calloc((size_t)(nbc > 0 ? nbc : 1), sizeof(double));
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t r = 0; r < R; ++r)
+            bwd_one_row(r, L, N, delta_softplus, u, delta, z, A, Dskip, dt_bias, h0, bidx, Bm, Cm,
+                        dy, dh_last, du, ddelta, dz, dA, dD, dbias, dh0, myB, myC);
+#pragma omp critical
+        for (int64_t i = 0; i < nbc; ++i) {
+            dB[i] += myB[i];
+            dC[i] += myC[i];
+        }
+        free(myB);
+        free(myC);
+    }
     return MBO_OK;
 }
 

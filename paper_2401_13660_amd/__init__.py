@@ -2,11 +2,13 @@
 
 The compute path is the HIP library ``libmbscan.so`` (hand-written gfx950
 kernels behind a C ABI declared in ``include/mbscan.h``); this package is a thin
-binding over it.  ``scan_fwd``, ``scan_step`` and the causal convolution upstream
+binding over it.  ``scan_fwd``, ``scan_step``, the backward ``scan_bwd``, the causal
+convolution upstream
 of the scan, ``conv1d`` and ``conv1d_step``, and the top-beta check that ends a
 speculative verification, ``verify_rank``, are loaded on first use.
 """
-__all__ = ["scan_fwd", "scan_step", "conv1d", "conv1d_step", "verify_rank", "load_library", "MBScanError"]
+__all__ = ["scan_fwd", "scan_step", "scan_bwd", "conv1d", "conv1d_step", "verify_rank", "load_library",
+           "MBScanError"]
 
 
 def __getattr__(name):

@@ -59,6 +59,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mb_conv1d_fwd.argtypes = [ctypes.POINTER(ConvDesc)] + [_VP] * 7
     lib.mb_conv1d_step.restype = ctypes.c_int
     lib.mb_conv1d_step.argtypes = [ctypes.c_int64] * 2 + [ctypes.c_int32] * 4 + [_VP] * 6
+    lib.mb_scan_bwd.restype = ctypes.c_int
+    lib.mb_scan_bwd.argtypes = [ctypes.POINTER(ScanDesc)] + [_VP] * 21
     lib.mb_verify_rank.restype = ctypes.c_int
     lib.mb_verify_rank.argtypes = [ctypes.c_int64] * 3 + [ctypes.c_int32] * 2 + [_VP] * 6
     lib.mb_status_string.restype = ctypes.c_char_p
@@ -296,3 +298,50 @@ def verify_rank(logits, draft, beta, *, return_ranks=False):
                                 _ptr(ranks), _ptr(accepted), _ptr(last_pos), stream)
     _check(st, "mb_verify_rank")
     return (accepted, last_pos, ranks) if return_ranks else (accepted, last_pos)
+
+
+def scan_bwd(u, delta, A, B, C, dy, D=None, dt_bias=None, z=None, h0=None, dh_last=None, *,
+             delta_softplus=True):
+    """Gradients of sum(dy * y) + sum(dh_last * h_last) for the scan of scan_fwd.
+
+    dy has y's dtype (fp32 or bf16), shape (batch, dim, L).  Returns a dict: du, ddelta,
+    dz (dy's dtype, (batch, dim, L); dz None without a gate), dA (dim, N), dB, dC
+    (batch, N, L), dD and dt_bias gradients ``dD``, ``ddt_bias`` (dim,) or None, and
+    dh0 (batch, dim, N), all fp32 but the first three.
+    """
+    lib = load_library()
+    if not isinstance(u, torch.Tensor) or u.dim() != 3:
+        raise MBScanError("u must be a (batch, dim, L) tensor")
+    nb, dim, L = u.shape
+    if not isinstance(A, torch.Tensor) or A.dim() != 2:
+        raise MBScanError("A must be a (dim, N) tensor")
+    N = A.shape[1]
+    dev, act = u.device, u.dtype
+    for t, name, shape, dt in ((u, "u", (nb, dim, L), act), (delta, "delta", (nb, dim, L), act),
+                               (A, "A", (dim, N), torch.float32), (B, "B", (nb, N, L), act),
+                               (C, "C", (nb, N, L), act), (dy, "dy", (nb, dim, L), None)):
+        _need(t, name, shape, dt, dev)
+    for t, name, shape, dt in ((z, "z", (nb, dim, L), act), (D, "D", (dim,), torch.float32),
+                               (dt_bias, "dt_bias", (dim,), torch.float32),
+                               (h0, "h0", (nb, dim, N), torch.float32),
+                               (dh_last, "dh_last", (nb, dim, N), torch.float32)):
+        if t is not None:
+            _need(t, name, shape, dt, dev)
+    f32 = dict(dtype=torch.float32, device=dev)
+    g = {"du": torch.empty((nb, dim, L), dtype=dy.dtype, device=dev),
+         "ddelta": torch.empty((nb, dim, L), dtype=dy.dtype, device=dev),
+         "dz": torch.empty((nb, dim, L), dtype=dy.dtype, device=dev) if z is not None else None,
+         "dA": torch.empty((dim, N), **f32), "dB": torch.empty((nb, N, L), **f32),
+         "dC": torch.empty((nb, N, L), **f32),
+         "dD": torch.empty(dim, **f32) if D is not None else None,
+         "ddt_bias": torch.empty(dim, **f32) if dt_bias is not None else None,
+         "dh0": torch.empty((nb, dim, N), **f32)}
+    desc = ScanDesc(nb, dim, L, N, _dt(act), _dt(dy.dtype), 1 if delta_softplus else 0, 0)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    with torch.cuda.device(dev):
+        st = lib.mb_scan_bwd(ctypes.byref(desc), _ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C), _ptr(D),
+                             _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(dy), _ptr(dh_last), _ptr(g["du"]),
+                             _ptr(g["ddelta"]), _ptr(g["dz"]), _ptr(g["dA"]), _ptr(g["dB"]), _ptr(g["dC"]),
+                             _ptr(g["dD"]), _ptr(g["ddt_bias"]), _ptr(g["dh0"]), stream)
+    _check(st, "mb_scan_bwd")
+    return g

@@ -8,6 +8,7 @@
 
 #include "conv1d.hpp"
 #include "mbscan.h"
+#include "scan_bwd.hpp"
 #include "scan_params.hpp"
 #include "scan_rowwise.hpp"
 #include "scan_step.hpp"
@@ -145,6 +146,55 @@ hipError_t conv_launch(mbs::conv::ConvParams &p, int32_t in_dtype, int32_t out_d
                                    : conv_dispatch<0, 1>(p, K, step, vec, stream);
     return out_dtype == MB_F32 ? conv_dispatch<1, 0>(p, K, step, vec, stream)
                                : conv_dispatch<1, 1>(p, K, step, vec, stream);
+}
+
+__global__ void zero_f32(float *p, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0.0f;
+}
+
+hipError_t zero_async(float *p, int64_t n, hipStream_t st) {
+    if (!p || n <= 0) return hipSuccess;
+    void *args[] = {&p, &n};
+    return hipLaunchKernel(reinterpret_cast<const void *>(&zero_f32), dim3((unsigned)((n + 255) / 256)),
+                           dim3(256), args, 0, st);
+}
+
+template <int IN, int OUT, bool GATE, bool SP>
+hipError_t bwd_launch(mbs::bwd::BwdParams &p, float *dA, float *dB, float *dC, float *dD, float *dbias,
+                      hipStream_t st) {
+    namespace W = mbs::bwd;
+    const int64_t n_cg = (p.dim + W::kCh - 1) / W::kCh;
+    const int64_t waves = n_cg * p.batch;
+    const dim3 grid((unsigned)((waves + W::kWaves - 1) / W::kWaves)), block(W::kThreads);
+    const size_t lds = sizeof(W::WaveSmem) * W::kWaves;
+    void *args[] = {&p};
+    hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_ckpt<IN, SP>), grid, block, args, lds,
+                                   st);
+    if (e != hipSuccess) return e;
+    e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_bwd<IN, OUT, GATE, SP>), grid, block, args, lds,
+                        st);
+    if (e != hipSuccess) return e;
+    int64_t ncg = n_cg;
+    void *fargs[] = {&p, &dB, &dC, &ncg};
+    const int64_t nbc = p.batch * p.seqlen * W::kQ;
+    e = hipLaunchKernel(reinterpret_cast<const void *>(&W::bwd_finish_bc), dim3((unsigned)((nbc + 255) / 256)),
+                        dim3(256), fargs, 0, st);
+    if (e != hipSuccess) return e;
+    void *rargs[] = {&p, &dA, &dD, &dbias};
+    const int64_t nr = p.dim * (W::kN + 2);
+    return hipLaunchKernel(reinterpret_cast<const void *>(&W::bwd_finish_rows), dim3((unsigned)((nr + 255) / 256)),
+                           dim3(256), rargs, 0, st);
+}
+
+template <int IN, int OUT>
+hipError_t bwd_dispatch(mbs::bwd::BwdParams &p, float *dA, float *dB, float *dC, float *dD, float *dbias,
+                        hipStream_t st) {
+    if (p.z)
+        return p.delta_softplus ? bwd_launch<IN, OUT, true, true>(p, dA, dB, dC, dD, dbias, st)
+                                : bwd_launch<IN, OUT, true, false>(p, dA, dB, dC, dD, dbias, st);
+    return p.delta_softplus ? bwd_launch<IN, OUT, false, true>(p, dA, dB, dC, dD, dbias, st)
+                            : bwd_launch<IN, OUT, false, false>(p, dA, dB, dC, dD, dbias, st);
 }
 
 }  // namespace
@@ -343,6 +393,97 @@ int mb_conv1d_step(int64_t batch, int64_t dim, int32_t width, int32_t in_dtype, 
     p.x = x_t; p.w = w; p.bias = bias; p.state_in = state; p.y = y_t; p.state_out = state;
     p.apply_silu = apply_silu ? 1 : 0;
     const hipError_t e = conv_launch(p, in_dtype, out_dtype, width, true, false, stream);
+    return e == hipSuccess ? MB_OK : MB_ERR_HIP;
+}
+
+int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
+                const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
+                const void *z, const float *h0, const void *dy, const float *dh_last,
+                void *du, void *ddelta, void *dz, float *dA, float *dB, float *dC, float *dDskip,
+                float *ddt_bias, float *dh0, void *stream) {
+    if (!desc) return MB_ERR_NULL;
+    const int64_t B = desc->batch, D = desc->dim, L = desc->seqlen, N = desc->dstate;
+    if (B < 0 || D < 0 || L < 0 || N < 0) return MB_ERR_SHAPE;
+    if (!valid_dtype(desc->in_dtype) || !valid_dtype(desc->out_dtype)) return MB_ERR_DTYPE;
+    if (desc->reserved != 0 || N != 16 || L % 16 != 0) return MB_ERR_UNSUPPORTED;
+    int64_t rows, elems, bc_elems, state_elems;
+    if (!mul_ok(B, D, &rows) || !mul_ok(rows, L, &elems) || !mul_ok(B * N, L, &bc_elems) ||
+        !mul_ok(rows, N, &state_elems))
+        return MB_ERR_SHAPE;
+    if (L >= (int64_t(1) << 31) || rows >= (int64_t(1) << 31)) return MB_ERR_SHAPE;
+    if (rows == 0) return MB_OK;
+    if (!A || !dA || (Dskip && !dDskip) || (dt_bias && !ddt_bias)) return MB_ERR_NULL;
+    if (L > 0 && (!u || !delta || !Bmat || !Cmat || !dy || !du || !ddelta || !dB || !dC || (z && !dz)))
+        return MB_ERR_NULL;
+    const size_t in_sz = dtype_size(desc->in_dtype), out_sz = dtype_size(desc->out_dtype);
+    const void *act_in[] = {u, delta, z, Bmat, Cmat};
+    for (const void *q : act_in)
+        if (q && !aligned(q, 16)) return MB_ERR_ALIGN;
+    const void *act_out[] = {dy, du, ddelta, dz};
+    for (const void *q : act_out)
+        if (q && !aligned(q, 16)) return MB_ERR_ALIGN;
+    const void *f32s[] = {A, Dskip, dt_bias, h0, dh_last, dA, dB, dC, dDskip, ddt_bias, dh0};
+    for (const void *q : f32s)
+        if (q && !aligned(q, 8)) return MB_ERR_ALIGN;
+    // outputs overlap nothing
+    const size_t in_b = (size_t)elems * in_sz, out_b = (size_t)elems * out_sz, bc_b = (size_t)bc_elems * in_sz;
+    const size_t st_b = (size_t)state_elems * 4, a_b = (size_t)(D * N) * 4, v_b = (size_t)D * 4;
+    struct Range { const void *p; size_t n; };
+    const Range ins[] = {{u, in_b}, {delta, in_b}, {z, in_b}, {Bmat, bc_b}, {Cmat, bc_b}, {A, a_b},
+                         {Dskip, v_b}, {dt_bias, v_b}, {h0, st_b}, {dy, out_b}, {dh_last, st_b}};
+    const Range outs[] = {{du, out_b}, {ddelta, out_b}, {dz, z ? out_b : 0}, {dA, a_b},
+                          {dB, (size_t)bc_elems * 4}, {dC, (size_t)bc_elems * 4}, {dDskip, v_b},
+                          {ddt_bias, v_b}, {dh0, st_b}};
+    const int n_out = sizeof(outs) / sizeof(outs[0]);
+    for (int i = 0; i < n_out; ++i) {
+        for (const Range &r : ins)
+            if (overlaps(outs[i].p, outs[i].n, r.p, r.n)) return MB_ERR_ALIAS;
+        for (int k = i + 1; k < n_out; ++k)
+            if (overlaps(outs[i].p, outs[i].n, outs[k].p, outs[k].n)) return MB_ERR_ALIAS;
+    }
+
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (L == 0) {
+        // no timestep: the state passes straight through; parameter gradients are zero
+        e = zero_async(dA, D * N, st);
+        if (e == hipSuccess) e = zero_async(dDskip, Dskip ? D : 0, st);
+        if (e == hipSuccess) e = zero_async(ddt_bias, dt_bias ? D : 0, st);
+        if (e == hipSuccess && dh0) {
+            void *args[] = {const_cast<float **>(&dh_last), &dh0, &state_elems};
+            e = hipLaunchKernel(reinterpret_cast<const void *>(&mbs::copy_state),
+                                dim3((unsigned)((state_elems + 255) / 256)), dim3(256), args, 0, st);
+        }
+        return e == hipSuccess ? MB_OK : MB_ERR_HIP;
+    }
+
+    namespace W = mbs::bwd;
+    const int64_t n_cg = (D + W::kCh - 1) / W::kCh;
+    const size_t ck_b = (size_t)(L / W::kT) * (size_t)rows * W::kN * 4;
+    const size_t bcp_b = (size_t)n_cg * (size_t)B * (size_t)L * W::kQ * 4 * 4;
+    const size_t row_b = (size_t)rows * (W::kN + 2) * 4;
+    char *ws = nullptr;
+    e = hipMallocAsync(reinterpret_cast<void **>(&ws), ck_b + bcp_b + row_b, st);
+    if (e != hipSuccess) return MB_ERR_HIP;
+    W::BwdParams p{};
+    p.batch = B; p.dim = D; p.seqlen = L;
+    p.u = u; p.delta = delta; p.Bm = Bmat; p.Cm = Cmat; p.z = z;
+    p.A = A; p.Dskip = Dskip; p.dt_bias = dt_bias; p.h0 = h0;
+    p.dy = dy; p.dh_last = dh_last;
+    p.du = du; p.ddelta = ddelta; p.dz = dz; p.dh0 = dh0;
+    p.ck = reinterpret_cast<float *>(ws);
+    p.part_bc = reinterpret_cast<float *>(ws + ck_b);
+    p.part_row = reinterpret_cast<float *>(ws + ck_b + bcp_b);
+    p.delta_softplus = desc->delta_softplus ? 1 : 0;
+    float *dD = Dskip ? dDskip : nullptr, *dbias = dt_bias ? ddt_bias : nullptr;
+    if (desc->in_dtype == MB_F32)
+        e = desc->out_dtype == MB_F32 ? bwd_dispatch<0, 0>(p, dA, dB, dC, dD, dbias, st)
+                                      : bwd_dispatch<0, 1>(p, dA, dB, dC, dD, dbias, st);
+    else
+        e = desc->out_dtype == MB_F32 ? bwd_dispatch<1, 0>(p, dA, dB, dC, dD, dbias, st)
+                                      : bwd_dispatch<1, 1>(p, dA, dB, dC, dD, dbias, st);
+    const hipError_t f = hipFreeAsync(ws, st);
+    if (e == hipSuccess) e = f;
     return e == hipSuccess ? MB_OK : MB_ERR_HIP;
 }
 

@@ -1,0 +1,384 @@
+// scan_bwd.hpp -- the backward of the selective scan (training, Section 4 and
+// Appendix C: MambaByte is trained at 8,192-byte contexts), for dstate 16.
+//
+// With lambda_t[n] the gradient of the loss with respect to h_t[n], reverse-mode
+// differentiation of eq. (2) with the discretisation of Appendix D and the
+// output and gating rows of Table 8 gives
+//
+//   ds_t        = dy_t g_t,  g_t = silu(z_t) (1 without a gate);  dz_t = dy_t s_t silu'(z_t)
+//   lambda_t[n] = ds_t C_t[n] + abar_{t+1}[n] lambda_{t+1}[n]        (+ dh_last at t = L-1)
+//   dC_t[n]    += ds_t h_t[n],   dB_t[n] += lambda_t[n] dlt_t u_t    (summed over channels)
+//   du_t        = ds_t Dskip + dlt_t sum_n lambda_t[n] B_t[n]
+//   ddlt_t      = sum_n lambda_t[n] (A[n] abar_t[n] h_{t-1}[n] + u_t B_t[n]);  ddelta = ddlt sigma(v)
+//   dA[n]      += dlt_t lambda_t[n] abar_t[n] h_{t-1}[n],  dDskip += ds_t u_t,  dbias += ddelta_t
+//   dh0[n]      = abar_0[n] lambda_0[n]
+//
+// Three kernels:
+//   scan_ckpt   forward recurrence (no output) storing h at the start of every
+//               16-step chunk: ck[(chunk * rows + row) * 16 + n];
+//   scan_bwd    the lanes of a wave own 8 channels x 16 states as in the forward
+//               kernel (lane 8j + q: channel j, states 2q, 2q+1).  Chunks run in
+//               reverse; per chunk: the per-element terms (A), the chunk's forward
+//               from its checkpoint keeping h_t and abar_t in VGPRs (F), s_t and
+//               dz (C1), the adjoint recurrence backwards (R), then du and ddelta
+//               (C2).  dB and dC are summed over the wave's 8 channels through
+//               LDS every 4 timesteps and written as one partial per wave;
+//   bwd_finish  sums the dB / dC partials over channel groups and dA, dDskip,
+//               dbias over the batch (no atomics: results are deterministic).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "device_math.hpp"
+#include "scan_params.hpp"
+
+#include <type_traits>
+
+namespace mbs {
+namespace bwd {
+
+constexpr int kN = 16;
+constexpr int kCh = 8;                 // channels per wave
+constexpr int kQ = 8;                  // lanes per channel
+constexpr int kT = 16;                 // timesteps per chunk
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * 64;
+
+struct BwdParams {
+    int64_t batch, dim, seqlen;
+    const void *u, *delta, *Bm, *Cm, *z;
+    const float *A, *Dskip, *dt_bias, *h0;
+    const void *dy;
+    const float *dh_last;
+    void *du, *ddelta, *dz;            // (batch, dim, L), out dtype
+    float *dh0;                        // (batch, dim, N) or null
+    // workspace
+    float *ck;                         // (L / 16, batch * dim, 16) checkpoints
+    float *part_bc;                    // (ncg, batch, L, 8, 4): per wave, summed over its channels
+    float *part_row;                   // (batch * dim, 16 + 2): dA (16), dDskip, dbias per row
+    int delta_softplus;
+};
+
+// 2 consecutive activations (4 bytes bf16, 8 bytes fp32).
+template <int DT> struct Raw2;
+template <> struct Raw2<1> {
+    uint32_t v;
+    __device__ __forceinline__ void load(const void *base, int64_t off) {
+        v = *reinterpret_cast<const uint32_t *>(static_cast<const uint16_t *>(base) + off);
+    }
+    __device__ __forceinline__ float get(int i) const { return i ? bf16_hi(v) : bf16_lo(v); }
+};
+template <> struct Raw2<0> {
+    u32x2 v;
+    __device__ __forceinline__ void load(const void *base, int64_t off) {
+        v = *reinterpret_cast<const u32x2 *>(static_cast<const float *>(base) + off);
+    }
+    __device__ __forceinline__ float get(int i) const { return __builtin_bit_cast(float, i ? v.y : v.x); }
+};
+
+template <int DT> __device__ __forceinline__ void store2(void *base, int64_t off, float a, float b) {
+    if (DT == 0) {
+        *reinterpret_cast<u32x2 *>(static_cast<float *>(base) + off) =
+            u32x2{__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b)};
+    } else {
+        *reinterpret_cast<uint32_t *>(static_cast<uint16_t *>(base) + off) =
+            (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+    }
+}
+
+// Private LDS area of one wave; padded rows keep reads and writes conflict-free.
+struct WaveSmem {
+    f32x4 dd[kT][kCh + 1];            // (dlt, dlt*u, ds, u) of timestep t, channel j
+    f32x4 bc[kT][kQ + 2];             // (B[2q], B[2q+1], C[2q], C[2q+1]) of timestep t
+    f32x4 pa[kCh * (kT / 4)][kQ + 1]; // per-state-pair partials, 4 timesteps per entry
+    f32x4 pb[kCh * (kT / 4)][kQ + 1];
+    f32x4 x[4][kQ][kCh + 1];          // dB / dC contributions of 4 timesteps, summed over j
+};
+
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The wave's (batch, channel group) from a workgroup renumbered so that each of
+// the 8 XCDs works on a contiguous range of groups.
+__device__ __forceinline__ int64_t wave_id() {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t per_xcd = (int64_t)gridDim.x / 8;
+    const int64_t k = blockIdx.x;
+    const int64_t lwg = k < per_xcd * 8 ? (k % 8) * per_xcd + k / 8 : k;
+    return lwg * kWaves + wave;
+}
+
+// ---- the checkpoint pass ------------------------------------------------------
+template <int IN, bool SOFTPLUS>
+__global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    WaveSmem &sm = reinterpret_cast<WaveSmem *>(smem_raw)[__builtin_amdgcn_readfirstlane(threadIdx.x >> 6)];
+    const int lane = threadIdx.x & 63, j = lane >> 3, q = lane & 7, n0 = 2 * q;
+    const int64_t n_cg = (p.dim + kCh - 1) / kCh;
+    const int64_t wid = wave_id();
+    if (wid >= n_cg * p.batch) return;
+    const int64_t cg = wid % n_cg, b = wid / n_cg;
+    const int64_t d = cg * kCh + j;
+    const bool live = d < p.dim;
+    const int64_t dcl = live ? d : p.dim - 1;
+    const int64_t row = b * p.dim + dcl, rows = p.batch * p.dim, L = p.seqlen;
+    const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
+    float a2[2], h[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        a2[s] = p.A[dcl * kN + n0 + s] * kLog2e;
+        h[s] = p.h0 ? p.h0[row * kN + n0 + s] : 0.0f;
+    }
+    const int64_t act = row * L, bcr = (b * kN + n0) * L;
+    for (int64_t t0 = 0; t0 < L; t0 += kT) {
+        // per element: lane (j, q) takes timesteps 2q, 2q+1; B staging: timesteps 2j, 2j+1
+        Raw2<IN> ru, rd, rb0, rb1;
+        ru.load(p.u, act + t0 + 2 * q);
+        rd.load(p.delta, act + t0 + 2 * q);
+        rb0.load(p.Bm, bcr + t0 + 2 * j);
+        rb1.load(p.Bm, bcr + L + t0 + 2 * j);
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const float v = rd.get(k) + bias;
+            const float dl = SOFTPLUS ? softplus_f32(v) : v;
+            sm.dd[2 * q + k][j] = f32x4{dl, dl * ru.get(k), 0.0f, 0.0f};
+            sm.bc[2 * j + k][q] = f32x4{rb0.get(k), rb1.get(k), 0.0f, 0.0f};
+        }
+        if (live)
+            *reinterpret_cast<u32x2 *>(p.ck + ((t0 / kT) * rows + row) * kN + n0) =
+                u32x2{__builtin_bit_cast(uint32_t, h[0]), __builtin_bit_cast(uint32_t, h[1])};
+        wave_sync();
+#pragma unroll
+        for (int t = 0; t < kT; ++t) {
+            const f32x4 dv = sm.dd[t][j];
+            const f32x4 bv = sm.bc[t][q];
+            h[0] = __builtin_fmaf(hw_exp2(dv.x * a2[0]), h[0], dv.y * bv.x);
+            h[1] = __builtin_fmaf(hw_exp2(dv.x * a2[1]), h[1], dv.y * bv.y);
+        }
+        wave_sync();
+    }
+}
+
+// ---- the backward pass -----------------------------------------------------------
+template <int IN, int OUT, bool GATE, bool SOFTPLUS>
+__global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    WaveSmem &sm = reinterpret_cast<WaveSmem *>(smem_raw)[__builtin_amdgcn_readfirstlane(threadIdx.x >> 6)];
+    const int lane = threadIdx.x & 63, j = lane >> 3, q = lane & 7, n0 = 2 * q;
+    const int64_t n_cg = (p.dim + kCh - 1) / kCh;
+    const int64_t wid = wave_id();
+    if (wid >= n_cg * p.batch) return;
+    const int64_t cg = wid % n_cg, b = wid / n_cg;
+    const int64_t d = cg * kCh + j;
+    const bool live = d < p.dim;
+    const int64_t dcl = live ? d : p.dim - 1;
+    const int64_t row = b * p.dim + dcl, rows = p.batch * p.dim, L = p.seqlen;
+    const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
+    const float dskip = p.Dskip ? p.Dskip[dcl] : 0.0f;
+    float a2[2], Av[2], carry[2], dA[2] = {0.0f, 0.0f};
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        Av[s] = p.A[dcl * kN + n0 + s];
+        a2[s] = Av[s] * kLog2e;
+        carry[s] = p.dh_last ? p.dh_last[row * kN + n0 + s] : 0.0f;      // abar_{t+1} lambda_{t+1}
+    }
+    float sum_dD = 0.0f, sum_dbias = 0.0f;
+    const int64_t act = row * L, bcr = (b * kN + n0) * L;
+    float *pbc = p.part_bc + ((cg * p.batch + b) * L) * (kQ * 4);
+
+    for (int64_t t0 = L - kT; t0 >= 0; t0 -= kT) {
+        // ---- A: per-element terms of timesteps 2q, 2q+1 and B/C staging ----------
+        Raw2<IN> ru, rd, rz, rb0, rb1, rc0, rc1;
+        Raw2<OUT> ry;
+        ru.load(p.u, act + t0 + 2 * q);
+        rd.load(p.delta, act + t0 + 2 * q);
+        if (GATE) rz.load(p.z, act + t0 + 2 * q);
+        ry.load(p.dy, act + t0 + 2 * q);
+        rb0.load(p.Bm, bcr + t0 + 2 * j);
+        rb1.load(p.Bm, bcr + L + t0 + 2 * j);
+        rc0.load(p.Cm, bcr + t0 + 2 * j);
+        rc1.load(p.Cm, bcr + L + t0 + 2 * j);
+        const float *ckp = p.ck + ((t0 / kT) * rows + row) * kN + n0;
+        float hb[kT + 1][2], ab[kT][2];                 // h_{t-1} .. h_{t+15}; abar_t
+        hb[0][0] = ckp[0];
+        hb[0][1] = ckp[1];
+        float xs[2], dyv[2], zv[2], sg[2], dlv[2], dsv[2];
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const float x = ru.get(k);
+            const float v = rd.get(k) + bias;
+            const float dl = SOFTPLUS ? softplus_f32(v) : v;
+            sg[k] = SOFTPLUS ? hw_rcp(1.0f + hw_exp2(-v * kLog2e)) : 1.0f;   // softplus'(v)
+            dyv[k] = ry.get(k);
+            zv[k] = GATE ? rz.get(k) : 0.0f;
+            const float g = GATE ? silu_f32(zv[k]) : 1.0f;
+            const float ds = dyv[k] * g;
+            xs[k] = x;
+            dlv[k] = dl;
+            dsv[k] = ds;
+            sum_dD = __builtin_fmaf(ds, x, sum_dD);
+            sm.dd[2 * q + k][j] = f32x4{dl, dl * x, ds, x};
+            sm.bc[2 * j + k][q] = f32x4{rb0.get(k), rb1.get(k), rc0.get(k), rc1.get(k)};
+        }
+        wave_sync();
+
+        // ---- F: the chunk's forward from its checkpoint -------------------------
+#pragma unroll
+        for (int tq = 0; tq < kT / 4; ++tq) {
+            float acc[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int t = 4 * tq + k;
+                const f32x4 dv = sm.dd[t][j];
+                const f32x4 bv = sm.bc[t][q];
+#pragma unroll
+                for (int s = 0; s < 2; ++s) {
+                    ab[t][s] = hw_exp2(dv.x * a2[s]);
+                    hb[t + 1][s] = __builtin_fmaf(ab[t][s], hb[t][s], dv.y * bv[s]);
+                }
+                acc[k] = __builtin_fmaf(bv.w, hb[t + 1][1], bv.z * hb[t + 1][0]);
+            }
+            sm.pa[4 * j + tq][q] = f32x4{acc[0], acc[1], acc[2], acc[3]};
+        }
+        wave_sync();
+
+        // ---- C1: s_t = C_t . h_t + Dskip u_t and dz for timesteps 2q, 2q+1 -------
+        if (GATE) {
+            float dzv[2];
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                const int t = 2 * q + k;
+                float s = 0.0f;
+#pragma unroll
+                for (int w = 0; w < kQ; ++w) s += sm.pa[4 * j + (t >> 2)][w][t & 3];
+                s = __builtin_fmaf(dskip, xs[k], s);
+                const float sgz = hw_rcp(1.0f + hw_exp2(-zv[k] * kLog2e));
+                dzv[k] = dyv[k] * s * sgz * __builtin_fmaf(zv[k], 1.0f - sgz, 1.0f);
+            }
+            if (live) store2<OUT>(p.dz, act + t0 + 2 * q, dzv[0], dzv[1]);
+        }
+        wave_sync();                                    // pa is rewritten below
+
+        // ---- R: the adjoint recurrence, timesteps 15 .. 0 -------------------------
+#pragma unroll
+        for (int tq = kT / 4 - 1; tq >= 0; --tq) {
+            float pu[4], pd[4];
+#pragma unroll
+            for (int k = 3; k >= 0; --k) {
+                const int t = 4 * tq + k;
+                const f32x4 dv = sm.dd[t][j];          // (dlt, dlt*u, ds, u)
+                const f32x4 bv = sm.bc[t][q];          // (B0, B1, C0, C1)
+                const float lam0 = __builtin_fmaf(dv.z, bv.z, carry[0]);
+                const float lam1 = __builtin_fmaf(dv.z, bv.w, carry[1]);
+                // a dead lane reads the last channel again: it must not add to dB / dC
+                sm.x[k][q][j] = live ? f32x4{lam0 * dv.y, lam1 * dv.y, dv.z * hb[t + 1][0], dv.z * hb[t + 1][1]}
+                                     : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                const float u0 = __builtin_fmaf(lam1, bv.y, lam0 * bv.x);
+                const float w0 = lam0 * ab[t][0] * hb[t][0];
+                const float w1 = lam1 * ab[t][1] * hb[t][1];
+                pu[k] = u0;
+                pd[k] = __builtin_fmaf(dv.w, u0, __builtin_fmaf(Av[1], w1, Av[0] * w0));
+                dA[0] = __builtin_fmaf(dv.x, w0, dA[0]);
+                dA[1] = __builtin_fmaf(dv.x, w1, dA[1]);
+                carry[0] = lam0 * ab[t][0];
+                carry[1] = lam1 * ab[t][1];
+            }
+            sm.pa[4 * j + tq][q] = f32x4{pu[0], pu[1], pu[2], pu[3]};
+            sm.pb[4 * j + tq][q] = f32x4{pd[0], pd[1], pd[2], pd[3]};
+            wave_sync();
+            // dB / dC of timesteps 4tq .. 4tq+3 summed over the wave's 8 channels:
+            // lane (half, k, q') sums channels 4 half .. 4 half + 3, the halves meet
+            // through a lane exchange, and half 0 writes 16 bytes of the partial.
+            {
+                const int half = lane >> 5, kk = (lane >> 3) & 3, qq = lane & 7;
+                f32x4 sum = sm.x[kk][qq][4 * half];
+#pragma unroll
+                for (int i = 1; i < 4; ++i) sum += sm.x[kk][qq][4 * half + i];
+#pragma unroll
+                for (int c = 0; c < 4; ++c) sum[c] += __shfl_xor(sum[c], 32, 64);
+                if (half == 0)
+                    *reinterpret_cast<f32x4 *>(pbc + ((t0 + 4 * tq + kk) * kQ + qq) * 4) = sum;
+            }
+            wave_sync();                                // x is rewritten by the next step
+        }
+
+        // ---- C2: du and ddelta of timesteps 2q, 2q+1 ------------------------------
+        {
+            float duv[2], ddv[2];
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                const int t = 2 * q + k;
+                float su = 0.0f, sd = 0.0f;
+#pragma unroll
+                for (int w = 0; w < kQ; ++w) {
+                    su += sm.pa[4 * j + (t >> 2)][w][t & 3];
+                    sd += sm.pb[4 * j + (t >> 2)][w][t & 3];
+                }
+                duv[k] = __builtin_fmaf(dlv[k], su, dsv[k] * dskip);
+                ddv[k] = sd * sg[k];
+                sum_dbias += ddv[k];
+            }
+            if (live) {
+                store2<OUT>(p.du, act + t0 + 2 * q, duv[0], duv[1]);
+                store2<OUT>(p.ddelta, act + t0 + 2 * q, ddv[0], ddv[1]);
+            }
+        }
+        wave_sync();                                    // dd / bc / pa / pb are rewritten
+    }
+
+    // ---- per-row results: dh0, dA (per state), dDskip and dbias (per channel) ----
+#pragma unroll
+    for (int off = 1; off < kQ; off <<= 1) {            // sum over the 8 lanes of channel j
+        sum_dD += __shfl_xor(sum_dD, off, 64);
+        sum_dbias += __shfl_xor(sum_dbias, off, 64);
+    }
+    if (live) {
+        if (p.dh0) {
+            p.dh0[row * kN + n0] = carry[0];
+            p.dh0[row * kN + n0 + 1] = carry[1];
+        }
+        float *pr = p.part_row + row * (kN + 2);
+        pr[n0] = dA[0];
+        pr[n0 + 1] = dA[1];
+        if (q == 0) {
+            pr[kN] = sum_dD;
+            pr[kN + 1] = sum_dbias;
+        }
+    }
+}
+
+// ---- the reductions ---------------------------------------------------------------
+// dB[b][n][t], dC[b][n][t]: thread (b, t, q) sums the ncg channel-group partials.
+__global__ __launch_bounds__(256) void bwd_finish_bc(BwdParams p, float *dB, float *dC, int64_t ncg) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;   // (b, t, q)
+    const int64_t L = p.seqlen;
+    if (i >= p.batch * L * kQ) return;
+    const int64_t qq = i % kQ, t = (i / kQ) % L, b = i / (kQ * L);
+    const int64_t stride = p.batch * L * kQ * 4;
+    const float *src = p.part_bc + ((b * L + t) * kQ + qq) * 4;
+    f32x4 sum = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int64_t c = 0; c < ncg; ++c) sum += *reinterpret_cast<const f32x4 *>(src + c * stride);
+    const int64_t n0 = 2 * qq;
+    dB[(b * kN + n0) * L + t] = sum.x;
+    dB[(b * kN + n0 + 1) * L + t] = sum.y;
+    dC[(b * kN + n0) * L + t] = sum.z;
+    dC[(b * kN + n0 + 1) * L + t] = sum.w;
+}
+
+// dA[d][n], dDskip[d], dbias[d]: thread (d, slot) sums over the batch.
+__global__ __launch_bounds__(256) void bwd_finish_rows(BwdParams p, float *dA, float *dD, float *dbias) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;   // (d, slot)
+    if (i >= p.dim * (kN + 2)) return;
+    const int64_t d = i / (kN + 2), slot = i % (kN + 2);
+    float sum = 0.0f;
+    for (int64_t b = 0; b < p.batch; ++b) sum += p.part_row[(b * p.dim + d) * (kN + 2) + slot];
+    if (slot < kN) dA[d * kN + slot] = sum;
+    else if (slot == kN) { if (dD) dD[d] = sum; }
+    else if (dbias) dbias[d] = sum;
+}
+
+}  // namespace bwd
+}  // namespace mbs

@@ -31,14 +31,14 @@ def test_exports_every_declared_symbol():
     lib = mb.load_library()
     names = declared_functions()
     assert {"mb_scan_fwd", "mb_scan_fwd_states", "mb_scan_step", "mb_conv1d_fwd", "mb_conv1d_step",
-            "mb_verify_rank", "mb_status_string", "mb_abi_version"} <= set(names)
+            "mb_verify_rank", "mb_scan_bwd", "mb_status_string", "mb_abi_version"} <= set(names)
     for n in names:
         assert hasattr(lib, n), f"{n} declared in mbscan.h but not exported"
 
 
 def test_version_and_status_strings():
     lib = mb.load_library()
-    assert lib.mb_abi_version() == 4
+    assert lib.mb_abi_version() == 5
     for code in range(-7, 1):
         assert lib.mb_status_string(code)
     assert lib.mb_status_string(-99) == b"unknown status"

@@ -1,0 +1,120 @@
+"""GPU parity of mb_scan_bwd against the fp64 oracle's backward.
+
+Every gradient is compared on the same input bits under the metric of
+tests/parity.py.  Bars (fp32 arithmetic and fp32 gradients, against the fp64
+oracle): 1e-4 for the per-element gradients du, ddelta, dz, for dB and dC
+(sums over channels) and for dh0; 2e-4 for dA, dDskip and dbias, which sum
+over every (batch, time) of a channel (up to 32,768 terms at the 972M layer
+shape, where 2e-5 is observed).  A bf16 gradient output adds one bf16
+rounding (2^-8).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import announce, dev_tensor, has_gpu
+from parity import rel_err
+from paper_2401_13660_amd.inputs import make_inputs, workload
+
+pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not has_gpu(), reason="needs a GPU")]
+
+TOL = dict(du=1e-4, ddelta=1e-4, dz=1e-4, dB=1e-4, dC=1e-4, dA=2e-4, dD=2e-4, ddt_bias=2e-4, dh0=1e-4)
+ORACLE_NAME = dict(du="du", ddelta="ddelta", dz="dz", dA="dA", dB="dB", dC="dC", dD="dD", ddt_bias="dbias",
+                   dh0="dh0")
+
+
+def grads_case(inp, *, with_dhl=True, out_dtype=torch.float32, delta_softplus=True, seed=60, rows=None):
+    import paper_2401_13660_amd as mb
+    t = {k: dev_tensor(v) for k, v in inp.arrays().items()}
+    rng = np.random.default_rng(seed)
+    dy = rng.standard_normal(inp.u.shape).astype(np.float32)
+    if out_dtype == torch.bfloat16:
+        from paper_2401_13660_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits
+        dy_bits = f32_to_bf16_bits(dy).reshape(dy.shape)
+        dy = bf16_bits_to_f32(dy_bits).reshape(dy.shape)
+        dy_dev = dev_tensor(dy_bits)
+    else:
+        dy_dev = dev_tensor(dy)
+    dhl = rng.standard_normal((inp.batch, inp.dim, inp.dstate)).astype(np.float32) if with_dhl else None
+    g = mb.scan_bwd(t["u"], t["delta"], t["A"], t["B"], t["C"], dy_dev, D=t.get("Dskip"),
+                    dt_bias=t.get("dt_bias"), z=t.get("z"), h0=t.get("h0"), dh_last=dev_tensor(dhl),
+                    delta_softplus=delta_softplus)
+    torch.cuda.synchronize()
+    ref = oracle.default().scan_bwd(inp.u, inp.delta, inp.A, inp.B, inp.C, dy, z=inp.z, Dskip=inp.Dskip,
+                                    dt_bias=inp.dt_bias, h0=inp.h0, dh_last=dhl, delta_softplus=delta_softplus,
+                                    dtype=inp.dtype)
+    errs = {}
+    bf = out_dtype == torch.bfloat16
+    for k, gv in g.items():
+        r = ref[ORACLE_NAME[k]]
+        if gv is None or r is None:
+            assert (gv is None) == (r is None or k == "dh0"), k
+            continue
+        gv = gv.float().cpu().numpy().astype(np.float64)
+        if rows is not None and k in ("du", "ddelta", "dz", "dh0"):
+            gv = gv.reshape(inp.batch * inp.dim, -1)[rows]
+            r = r.reshape(inp.batch * inp.dim, -1)[rows]
+        errs[k] = rel_err(gv, r)
+    print("[bwd errors]", {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    for k, e in errs.items():
+        tol = TOL[k] + (2.0 ** -8 if bf and k in ("du", "ddelta", "dz") else 0.0)
+        assert e <= tol, f"{k}: relative error {e:.3e} > {tol:.1e}"
+    return errs
+
+
+# (batch, dim, L): one chunk; several chunks with a ragged channel count (dead
+# lanes in the last 8-channel group); long enough that the reverse carry runs far.
+@pytest.mark.parametrize("shape", [(2, 196, 16), (3, 100, 48), (2, 196, 1008)])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_bwd_shapes(shape, dtype):
+    inp = make_inputs(*shape, 16, dtype=dtype, seed=61, with_h0=True)
+    announce(f"bwd {shape} {dtype}")
+    grads_case(inp)
+
+
+@pytest.mark.parametrize("gated,with_h0,with_dhl", [(False, False, False), (True, False, True),
+                                                    (False, True, False)])
+def test_bwd_options(gated, with_h0, with_dhl):
+    inp = make_inputs(2, 64, 256, 16, dtype="bf16", seed=62, gated=gated, with_h0=with_h0)
+    announce(f"bwd gated={gated} h0={with_h0} dh_last={with_dhl}")
+    grads_case(inp, with_dhl=with_dhl)
+
+
+def test_bwd_no_skip_no_bias_no_softplus():
+    from paper_2401_13660_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits
+    inp = make_inputs(2, 64, 256, 16, dtype="bf16", seed=63, with_D=False, with_bias=False)
+    # without softplus Delta = delta_raw is used as given: keep it positive
+    vals = np.abs(bf16_bits_to_f32(inp.delta).reshape(inp.u.shape)) * 0.1 + 0.01
+    inp.delta = f32_to_bf16_bits(vals.astype(np.float32)).reshape(inp.u.shape)
+    announce("bwd no skip, no bias, no softplus")
+    grads_case(inp, delta_softplus=False)
+
+
+def test_bwd_random_A_and_bf16_gradients():
+    inp = make_inputs(2, 96, 512, 16, dtype="bf16", seed=64, with_h0=True, A_kind="random")
+    announce("bwd random A, bf16 dy and gradients")
+    grads_case(inp, out_dtype=torch.bfloat16)
+
+
+def test_bwd_deterministic():
+    import paper_2401_13660_amd as mb
+    inp = make_inputs(2, 128, 512, 16, dtype="bf16", seed=65, with_h0=True)
+    t = {k: dev_tensor(v) for k, v in inp.arrays().items()}
+    dy = torch.randn(inp.u.shape, generator=torch.Generator().manual_seed(0)).to("cuda:0")
+    announce("bwd determinism")
+    outs = [mb.scan_bwd(t["u"], t["delta"], t["A"], t["B"], t["C"], dy, D=t["Dskip"], dt_bias=t["dt_bias"],
+                        z=t["z"], h0=t["h0"]) for _ in range(2)]
+    torch.cuda.synchronize()
+    for k in outs[0]:
+        if outs[0][k] is not None:
+            assert torch.equal(outs[0][k], outs[1][k]), f"{k} differs between runs"
+
+
+def test_bwd_972m_layer_sampled_rows():
+    """The MambaByte-972M layer shape at full size: row gradients on sampled rows; dB, dC,
+    dA, dDskip, dbias in full (they sum over every row, so the oracle runs all rows)."""
+    inp = workload("mambabyte972m_L8192", seed=0)
+    rows = np.sort(np.random.default_rng(66).choice(inp.batch * inp.dim, 32, replace=False))
+    announce("bwd 972M layer (4, 3584, 8192)")
+    grads_case(inp, with_dhl=False, rows=rows)
