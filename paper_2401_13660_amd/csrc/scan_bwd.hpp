@@ -69,11 +69,13 @@ template <> struct Raw2<1> {
     __device__ __forceinline__ float get(int i) const { return i ? bf16_hi(v) : bf16_lo(v); }
 };
 template <> struct Raw2<0> {
-    u32x2 v;
+    float v0, v1;
     __device__ __forceinline__ void load(const void *base, int64_t off) {
-        v = *reinterpret_cast<const u32x2 *>(static_cast<const float *>(base) + off);
+        const float *f = static_cast<const float *>(base) + off;
+        v0 = f[0];
+        v1 = f[1];
     }
-    __device__ __forceinline__ float get(int i) const { return __builtin_bit_cast(float, i ? v.y : v.x); }
+    __device__ __forceinline__ float get(int i) const { return i ? v1 : v0; }
 };
 
 template <int DT> __device__ __forceinline__ void store2(void *base, int64_t off, float a, float b) {
@@ -101,6 +103,23 @@ __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Sum over the 8 state-pair lanes of channel j of the per-4-timestep partials in
+// part[4j + t/4][lane][t%4], for the lane's own timesteps t = 2q and 2q + 1 (the
+// two are adjacent in one entry, so each partial is one 8-byte read).
+__device__ __forceinline__ void part_sum(const f32x4 (&part)[kCh * (kT / 4)][kQ + 1], int j, int q,
+                                         float (&out)[2]) {
+    const float *base = reinterpret_cast<const float *>(&part[4 * j + (q >> 1)][0]) + 2 * (q & 1);
+    float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kQ; ++w) {
+        const float2 v = *reinterpret_cast<const float2 *>(base + 4 * w);
+        s0 += v.x;
+        s1 += v.y;
+    }
+    out[0] = s0;
+    out[1] = s1;
+}
+
 // The wave's (batch, channel group) from a workgroup renumbered so that each of
 // the 8 XCDs works on a contiguous range of groups.
 __device__ __forceinline__ int64_t wave_id() {
@@ -112,6 +131,8 @@ __device__ __forceinline__ int64_t wave_id() {
 }
 
 // ---- the checkpoint pass ------------------------------------------------------
+// Loads run two chunks ahead in two static register slots (clamped, never
+// branched), as in the forward kernel.
 template <int IN, bool SOFTPLUS>
 __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -133,20 +154,25 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
         h[s] = p.h0 ? p.h0[row * kN + n0 + s] : 0.0f;
     }
     const int64_t act = row * L, bcr = (b * kN + n0) * L;
-    for (int64_t t0 = 0; t0 < L; t0 += kT) {
-        // per element: lane (j, q) takes timesteps 2q, 2q+1; B staging: timesteps 2j, 2j+1
-        Raw2<IN> ru, rd, rb0, rb1;
-        ru.load(p.u, act + t0 + 2 * q);
-        rd.load(p.delta, act + t0 + 2 * q);
-        rb0.load(p.Bm, bcr + t0 + 2 * j);
-        rb1.load(p.Bm, bcr + L + t0 + 2 * j);
+
+    // per element: lane (j, q) takes timesteps 2q, 2q+1; B staging: timesteps 2j, 2j+1
+    struct Slot { Raw2<IN> u, dl, b0, b1; };
+    auto issue = [&](Slot &sl, int64_t t0) {
+        const int64_t tc = t0 < L ? t0 : L - kT;           // past the end: reload the last chunk
+        sl.u.load(p.u, act + tc + 2 * q);
+        sl.dl.load(p.delta, act + tc + 2 * q);
+        sl.b0.load(p.Bm, bcr + tc + 2 * j);
+        sl.b1.load(p.Bm, bcr + L + tc + 2 * j);
+    };
+    auto chunk = [&](Slot &sl, int64_t t0) {
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
-            const float v = rd.get(k) + bias;
+            const float v = sl.dl.get(k) + bias;
             const float dl = SOFTPLUS ? softplus_f32(v) : v;
-            sm.dd[2 * q + k][j] = f32x4{dl, dl * ru.get(k), 0.0f, 0.0f};
-            sm.bc[2 * j + k][q] = f32x4{rb0.get(k), rb1.get(k), 0.0f, 0.0f};
+            sm.dd[2 * q + k][j] = f32x4{dl, dl * sl.u.get(k), 0.0f, 0.0f};
+            sm.bc[2 * j + k][q] = f32x4{sl.b0.get(k), sl.b1.get(k), 0.0f, 0.0f};
         }
+        issue(sl, t0 + 2 * kT);
         if (live)
             *reinterpret_cast<u32x2 *>(p.ck + ((t0 / kT) * rows + row) * kN + n0) =
                 u32x2{__builtin_bit_cast(uint32_t, h[0]), __builtin_bit_cast(uint32_t, h[1])};
@@ -159,7 +185,16 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
             h[1] = __builtin_fmaf(hw_exp2(dv.x * a2[1]), h[1], dv.y * bv.y);
         }
         wave_sync();
+    };
+    Slot s0, s1;
+    issue(s0, 0);
+    issue(s1, kT);
+    int64_t t0 = 0;
+    for (; t0 + 2 * kT <= L; t0 += 2 * kT) {
+        chunk(s0, t0);
+        chunk(s1, t0 + kT);
     }
+    if (t0 < L) chunk(s0, t0);
 }
 
 // ---- the backward pass -----------------------------------------------------------
@@ -183,46 +218,61 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
     for (int s = 0; s < 2; ++s) {
         Av[s] = p.A[dcl * kN + n0 + s];
         a2[s] = Av[s] * kLog2e;
-        carry[s] = p.dh_last ? p.dh_last[row * kN + n0 + s] : 0.0f;      // abar_{t+1} lambda_{t+1}
+        carry[s] = (p.dh_last && live) ? p.dh_last[row * kN + n0 + s] : 0.0f;   // abar_{t+1} lambda_{t+1}
     }
     float sum_dD = 0.0f, sum_dbias = 0.0f;
     const int64_t act = row * L, bcr = (b * kN + n0) * L;
     float *pbc = p.part_bc + ((cg * p.batch + b) * L) * (kQ * 4);
 
-    for (int64_t t0 = L - kT; t0 >= 0; t0 -= kT) {
+    // Loads run two chunks ahead (in processing order: backwards in time) in two
+    // static register slots, clamped at the sequence start, never branched.
+    struct Slot {
+        Raw2<IN> u, dl, z, b0, b1, c0, c1;
+        Raw2<OUT> dy;
+        float ck0, ck1;
+    };
+    auto issue = [&](Slot &sl, int64_t t0) {
+        const int64_t tc = t0 >= 0 ? t0 : 0;
+        sl.u.load(p.u, act + tc + 2 * q);
+        sl.dl.load(p.delta, act + tc + 2 * q);
+        if (GATE) sl.z.load(p.z, act + tc + 2 * q);
+        sl.dy.load(p.dy, act + tc + 2 * q);
+        sl.b0.load(p.Bm, bcr + tc + 2 * j);
+        sl.b1.load(p.Bm, bcr + L + tc + 2 * j);
+        sl.c0.load(p.Cm, bcr + tc + 2 * j);
+        sl.c1.load(p.Cm, bcr + L + tc + 2 * j);
+        const float *ckp = p.ck + ((tc / kT) * rows + row) * kN + n0;
+        sl.ck0 = ckp[0];
+        sl.ck1 = ckp[1];
+    };
+
+    auto chunk = [&](Slot &sl, int64_t t0) {
         // ---- A: per-element terms of timesteps 2q, 2q+1 and B/C staging ----------
-        Raw2<IN> ru, rd, rz, rb0, rb1, rc0, rc1;
-        Raw2<OUT> ry;
-        ru.load(p.u, act + t0 + 2 * q);
-        rd.load(p.delta, act + t0 + 2 * q);
-        if (GATE) rz.load(p.z, act + t0 + 2 * q);
-        ry.load(p.dy, act + t0 + 2 * q);
-        rb0.load(p.Bm, bcr + t0 + 2 * j);
-        rb1.load(p.Bm, bcr + L + t0 + 2 * j);
-        rc0.load(p.Cm, bcr + t0 + 2 * j);
-        rc1.load(p.Cm, bcr + L + t0 + 2 * j);
-        const float *ckp = p.ck + ((t0 / kT) * rows + row) * kN + n0;
+        // A dead lane (channel beyond dim) starts from h = 0 with lambda = 0 and has
+        // dlt*u = ds = 0, so every term it computes is exactly 0 and it adds nothing
+        // to the dB / dC sums over channels.
         float hb[kT + 1][2], ab[kT][2];                 // h_{t-1} .. h_{t+15}; abar_t
-        hb[0][0] = ckp[0];
-        hb[0][1] = ckp[1];
+        hb[0][0] = live ? sl.ck0 : 0.0f;
+        hb[0][1] = live ? sl.ck1 : 0.0f;
         float xs[2], dyv[2], zv[2], sg[2], dlv[2], dsv[2];
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
-            const float x = ru.get(k);
-            const float v = rd.get(k) + bias;
+            const float x = sl.u.get(k);
+            const float v = sl.dl.get(k) + bias;
             const float dl = SOFTPLUS ? softplus_f32(v) : v;
             sg[k] = SOFTPLUS ? hw_rcp(1.0f + hw_exp2(-v * kLog2e)) : 1.0f;   // softplus'(v)
-            dyv[k] = ry.get(k);
-            zv[k] = GATE ? rz.get(k) : 0.0f;
+            dyv[k] = sl.dy.get(k);
+            zv[k] = GATE ? sl.z.get(k) : 0.0f;
             const float g = GATE ? silu_f32(zv[k]) : 1.0f;
             const float ds = dyv[k] * g;
             xs[k] = x;
             dlv[k] = dl;
             dsv[k] = ds;
             sum_dD = __builtin_fmaf(ds, x, sum_dD);
-            sm.dd[2 * q + k][j] = f32x4{dl, dl * x, ds, x};
-            sm.bc[2 * j + k][q] = f32x4{rb0.get(k), rb1.get(k), rc0.get(k), rc1.get(k)};
+            sm.dd[2 * q + k][j] = live ? f32x4{dl, dl * x, ds, x} : f32x4{dl, 0.0f, 0.0f, x};
+            sm.bc[2 * j + k][q] = f32x4{sl.b0.get(k), sl.b1.get(k), sl.c0.get(k), sl.c1.get(k)};
         }
+        issue(sl, t0 - 2 * kT);                         // refill with the chunk two further back
         wave_sync();
 
         // ---- F: the chunk's forward from its checkpoint -------------------------
@@ -247,14 +297,11 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
 
         // ---- C1: s_t = C_t . h_t + Dskip u_t and dz for timesteps 2q, 2q+1 -------
         if (GATE) {
-            float dzv[2];
+            float dzv[2], sp[2];
+            part_sum(sm.pa, j, q, sp);
 #pragma unroll
             for (int k = 0; k < 2; ++k) {
-                const int t = 2 * q + k;
-                float s = 0.0f;
-#pragma unroll
-                for (int w = 0; w < kQ; ++w) s += sm.pa[4 * j + (t >> 2)][w][t & 3];
-                s = __builtin_fmaf(dskip, xs[k], s);
+                const float s = __builtin_fmaf(dskip, xs[k], sp[k]);
                 const float sgz = hw_rcp(1.0f + hw_exp2(-zv[k] * kLog2e));
                 dzv[k] = dyv[k] * s * sgz * __builtin_fmaf(zv[k], 1.0f - sgz, 1.0f);
             }
@@ -273,14 +320,12 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
                 const f32x4 bv = sm.bc[t][q];          // (B0, B1, C0, C1)
                 const float lam0 = __builtin_fmaf(dv.z, bv.z, carry[0]);
                 const float lam1 = __builtin_fmaf(dv.z, bv.w, carry[1]);
-                // a dead lane reads the last channel again: it must not add to dB / dC
-                sm.x[k][q][j] = live ? f32x4{lam0 * dv.y, lam1 * dv.y, dv.z * hb[t + 1][0], dv.z * hb[t + 1][1]}
-                                     : f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+                sm.x[k][q][j] = f32x4{lam0 * dv.y, lam1 * dv.y, dv.z * hb[t + 1][0], dv.z * hb[t + 1][1]};
                 const float u0 = __builtin_fmaf(lam1, bv.y, lam0 * bv.x);
                 const float w0 = lam0 * ab[t][0] * hb[t][0];
                 const float w1 = lam1 * ab[t][1] * hb[t][1];
-                pu[k] = u0;
-                pd[k] = __builtin_fmaf(dv.w, u0, __builtin_fmaf(Av[1], w1, Av[0] * w0));
+                pu[k] = u0;                             // sum_n lambda B      (du; u * it in ddelta)
+                pd[k] = __builtin_fmaf(Av[1], w1, Av[0] * w0);   // sum_n A lambda abar h_{t-1}
                 dA[0] = __builtin_fmaf(dv.x, w0, dA[0]);
                 dA[1] = __builtin_fmaf(dv.x, w1, dA[1]);
                 carry[0] = lam0 * ab[t][0];
@@ -307,18 +352,13 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
 
         // ---- C2: du and ddelta of timesteps 2q, 2q+1 ------------------------------
         {
-            float duv[2], ddv[2];
+            float duv[2], ddv[2], su[2], sd[2];
+            part_sum(sm.pa, j, q, su);
+            part_sum(sm.pb, j, q, sd);
 #pragma unroll
             for (int k = 0; k < 2; ++k) {
-                const int t = 2 * q + k;
-                float su = 0.0f, sd = 0.0f;
-#pragma unroll
-                for (int w = 0; w < kQ; ++w) {
-                    su += sm.pa[4 * j + (t >> 2)][w][t & 3];
-                    sd += sm.pb[4 * j + (t >> 2)][w][t & 3];
-                }
-                duv[k] = __builtin_fmaf(dlv[k], su, dsv[k] * dskip);
-                ddv[k] = sd * sg[k];
+                duv[k] = __builtin_fmaf(dlv[k], su[k], dsv[k] * dskip);
+                ddv[k] = __builtin_fmaf(xs[k], su[k], sd[k]) * sg[k];
                 sum_dbias += ddv[k];
             }
             if (live) {
@@ -327,7 +367,17 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
             }
         }
         wave_sync();                                    // dd / bc / pa / pb are rewritten
+    };
+
+    Slot s0, s1;
+    issue(s0, L - kT);
+    issue(s1, L - 2 * kT);
+    int64_t t0 = L - kT;
+    for (; t0 - kT >= 0; t0 -= 2 * kT) {               // pairs of chunks, backwards
+        chunk(s0, t0);
+        chunk(s1, t0 - kT);
     }
+    if (t0 >= 0) chunk(s0, t0);
 
     // ---- per-row results: dh0, dA (per state), dDskip and dbias (per channel) ----
 #pragma unroll
