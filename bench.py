@@ -44,6 +44,7 @@ ALU_PEAK_GELEMS = 1024 * 2.4e9 / ALU_SIMD_CYCLES_PER_ELEMENT / 1e9
 # operations (ds, dz, du, ddelta, the dDskip and dbias sums, dlt * u).
 BWD_SIMD_CYCLES_PER_ELEMENT = ((16 + 5) * 4 + (16 * 14 + 16) * 2) / 64.0
 BWD_ALU_PEAK_GELEMS = 1024 * 2.4e9 / BWD_SIMD_CYCLES_PER_ELEMENT / 1e9
+TRAIN_ALU_PEAK_GELEMS = 1024 * 2.4e9 / (ALU_SIMD_CYCLES_PER_ELEMENT + BWD_SIMD_CYCLES_PER_ELEMENT) / 1e9
 METRIC = "selective-scan GB/s & %HBM peak (972M layer, L=8192); B·L·D elems/s"
 DEFAULT_WORKLOAD = "mambabyte972m_L8192"
 from paper_2401_13660_amd.profile_summary import (  # noqa: E402
@@ -208,10 +209,12 @@ def bwd_bytes(inp) -> int:
     return int(b)
 
 
-def bench_bwd(args):
+def bench_bwd(args, train=False):
     """One mb_scan_bwd per step over the workload: the backward of the scan in the
     training setting (bf16 activations and incoming gradient, bf16 activation
-    gradients, fp32 parameter gradients)."""
+    gradients, fp32 parameter gradients).  ``train``: a step is the training pair,
+    the forward that stores the checkpoints (bf16 y) and the backward that reads
+    them."""
     import torch
 
     import paper_2401_13660_amd as mb
@@ -230,9 +233,15 @@ def bench_bwd(args):
     g = {k: t(v) for k, v in inp.arrays().items()}
     dy = torch.randn(inp.u.shape, generator=torch.Generator().manual_seed(1)).to(dev).to(torch.bfloat16)
 
+    kw = dict(D=g.get("Dskip"), dt_bias=g.get("dt_bias"), z=g.get("z"), h0=g.get("h0"))
+    y_buf = torch.empty(inp.u.shape, dtype=torch.bfloat16, device=dev)
+    ck_buf = torch.empty((inp.seqlen // 16, inp.batch, inp.dim, inp.dstate), dtype=torch.float32, device=dev)
+
     def step():
-        return mb.scan_bwd(g["u"], g["delta"], g["A"], g["B"], g["C"], dy, D=g.get("Dskip"),
-                           dt_bias=g.get("dt_bias"), z=g.get("z"), h0=g.get("h0"))
+        if not train:
+            return mb.scan_bwd(g["u"], g["delta"], g["A"], g["B"], g["C"], dy, **kw)
+        mb.scan_fwd(g["u"], g["delta"], g["A"], g["B"], g["C"], out=y_buf, ck=ck_buf, **kw)
+        return mb.scan_bwd(g["u"], g["delta"], g["A"], g["B"], g["C"], dy, ck=ck_buf, **kw)
 
     for _ in range(args.warmup):
         step()
@@ -248,20 +257,22 @@ def bench_bwd(args):
     nbytes = bwd_bytes(inp)
     gbs = nbytes / (ms * 1e-3) / 1e9
     gel = E / (ms * 1e-3) / 1e9
+    peak = TRAIN_ALU_PEAK_GELEMS if train else BWD_ALU_PEAK_GELEMS
+    what = "forward + backward (training pair)" if train else "backward"
     line = {
-        "metric": f"selective-scan backward: B·L·D elems/s ({args.workload})",
+        "metric": f"selective-scan {what}: B·L·D elems/s ({args.workload})",
         "value": round(E / (ms * 1e-3), 1), "unit": "elems/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": args.workload, "mode": "bwd",
+        "config": {"workload": args.workload, "mode": "train" if train else "bwd",
                    **{k: v for k, v in WORKLOADS[args.workload].items()},
                    "dy_dtype": "bf16", "grad_dtype": "bf16 (activations), f32 (parameters, dB, dC)",
                    "parallelism": "single GPU"},
         # the whole call (checkpoint pass, backward, two reductions) against the
         # backward's ALU minimum; its HBM side for comparison
-        "roofline": {"bound": "alu", "achieved": round(gel, 2), "peak": round(BWD_ALU_PEAK_GELEMS, 1),
-                     "unit": "Gelem/s", "frac": round(gel / BWD_ALU_PEAK_GELEMS, 4), "traffic": None,
-                     "scope": "whole mb_scan_bwd call", "hbm_gbs": round(gbs, 1),
+        "roofline": {"bound": "alu", "achieved": round(gel, 2), "peak": round(peak, 1),
+                     "unit": "Gelem/s", "frac": round(gel / peak, 4), "traffic": None,
+                     "scope": "whole step: every kernel of the call(s)", "hbm_gbs": round(gbs, 1),
                      "hbm_frac": round(gbs / HBM_PEAK_GBS, 4), "algorithmic_bytes": nbytes},
     }
     if not args.no_cpu_baseline:
@@ -277,6 +288,9 @@ def bench_bwd(args):
                                   C=cut(inp.C), h0=cut(inp.h0))
         dy_bits = dy[:nb].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
         t0 = time.perf_counter()
+        if train:                                   # the oracle's forward is part of the pair
+            orc.scan_fwd(sub.u, sub.delta, sub.A, sub.B, sub.C, z=sub.z, Dskip=sub.Dskip, dt_bias=sub.dt_bias,
+                         h0=sub.h0, dtype=sub.dtype)
         ref = orc.scan_bwd(sub.u, sub.delta, sub.A, sub.B, sub.C, dy_bits, z=sub.z, Dskip=sub.Dskip,
                            dt_bias=sub.dt_bias, h0=sub.h0, dtype=sub.dtype)
         elapsed = time.perf_counter() - t0
@@ -361,17 +375,18 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["fwd", "step", "conv", "rank", "bwd"], default="fwd",
+    ap.add_argument("--mode", choices=["fwd", "step", "conv", "rank", "bwd", "train"], default="fwd",
                     help="fwd: one mb_scan_fwd per step; step: seqlen successive mb_scan_step calls per step "
                          "(the recurrent-generation form of the same workload); conv: one mb_conv1d_fwd "
                          "(the causal convolution + Swish in front of the scan, k = 4, bf16 out); rank: one "
                          "mb_verify_rank (top-3 check of 16 drafted bytes over 256-way logits, batch 32); "
-                         "bwd: one mb_scan_bwd (bf16 dy and activation gradients, fp32 parameter gradients)")
+                         "bwd: one mb_scan_bwd (bf16 dy and activation gradients, fp32 parameter gradients); "
+                         "train: one mb_scan_fwd_ckpt (bf16 y) and one mb_scan_bwd from its checkpoints")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the scan, run a plain device copy of MIB MiB (reference for HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+        print(f"bench.py runs on one GPU only: there is no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
         sys.exit(2)
 
@@ -395,8 +410,8 @@ def main():
         return bench_conv(args)
     if args.mode == "rank":
         return bench_rank(args)
-    if args.mode == "bwd":
-        return bench_bwd(args)
+    if args.mode in ("bwd", "train"):
+        return bench_bwd(args, train=args.mode == "train")
 
     inp = workload(args.workload, seed=0)
     dev = torch.device("cuda:0")

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define MB_ABI_VERSION 5
+#define MB_ABI_VERSION 6
 
 typedef enum {
     MB_F32 = 0,
@@ -140,6 +140,27 @@ int mb_scan_fwd_states(const mb_scan_desc *desc,
                        const int32_t *pos, int64_t npos, float *h_pos, void *stream);
 
 /*
+ * mb_scan_fwd that also stores the checkpoints mb_scan_bwd recomputes its
+ * chunks from: the training forward (Section 4, Appendix C), whose backward
+ * then skips its own forward pass over the sequence.
+ *
+ *   ck     float (L/16, B, D, N)   ck[k][b][d][n] = h_{16k-1}[n] of row (b, d),
+ *                                  the state before timestep 16k (h0, or zeros,
+ *                                  for k = 0).  Required; must not overlap any
+ *                                  other argument; 8-byte aligned.
+ *
+ * Every other argument is as for mb_scan_fwd, and y and h_last are the same
+ * bits as mb_scan_fwd's.  Supported: dstate 16, L a multiple of 16 below 2^25
+ * (MB_ERR_UNSUPPORTED otherwise), u, delta, z, Bmat, Cmat and y 16-byte
+ * aligned (MB_ERR_ALIGN otherwise).
+ */
+int mb_scan_fwd_ckpt(const mb_scan_desc *desc,
+                     const void *u, const void *delta, const float *A,
+                     const void *Bmat, const void *Cmat,
+                     const float *Dskip, const float *dt_bias, const void *z,
+                     const float *h0, void *y, float *h_last, float *ck, void *stream);
+
+/*
  * One recurrent step per row, the state updated in place (Section 2:
  * generation runs the recurrence directly; Algorithm 1's byte-level
  * correction loop).  Identical to mb_scan_fwd with L = 1, h0 = h_last = h.
@@ -168,6 +189,9 @@ int mb_scan_step(int64_t batch, int64_t dim, int64_t dstate,
  *   desc, u, delta, A, Bmat, Cmat, Dskip, dt_bias, z, h0   as for mb_scan_fwd
  *   dy        out-dtype (B, D, L)   gradient with respect to y (desc->out_dtype)
  *   dh_last   float (B, D, N)       gradient with respect to h_last; NULL means 0
+ *   ck        float (L/16, B, D, N) checkpoints written by mb_scan_fwd_ckpt for
+ *                                   the same inputs, read only; NULL: the call
+ *                                   computes them itself (one more forward pass)
  *   du, ddelta, dz   out-dtype (B, D, L)   dz is required when z is given
  *   dA        float (D, N)          summed over batch and time
  *   dB, dC    float (B, N, L)       summed over the channels of each batch element
@@ -178,14 +202,14 @@ int mb_scan_step(int64_t batch, int64_t dim, int64_t dstate,
  * 16-byte aligned and every float pointer 8-byte aligned (MB_ERR_UNSUPPORTED /
  * MB_ERR_ALIGN otherwise).  Results are deterministic.  The call allocates a
  * stream-ordered workspace (hipMallocAsync): state checkpoints every 16 bytes
- * (L/16 x B x D x 16 floats) and per-8-channel dB/dC partials (B x L x D/8 x 64
- * bytes), freed on the same stream.
+ * (L/16 x B x D x 16 floats, only when ck is NULL) and per-8-channel dB/dC
+ * partials (B x L x D/8 x 64 bytes), freed on the same stream.
  */
 int mb_scan_bwd(const mb_scan_desc *desc,
                 const void *u, const void *delta, const float *A,
                 const void *Bmat, const void *Cmat,
                 const float *Dskip, const float *dt_bias, const void *z,
-                const float *h0, const void *dy, const float *dh_last,
+                const float *h0, const void *dy, const float *dh_last, const float *ck,
                 void *du, void *ddelta, void *dz, float *dA, float *dB, float *dC,
                 float *dDskip, float *ddt_bias, float *dh0, void *stream);
 

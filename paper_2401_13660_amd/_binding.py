@@ -60,7 +60,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mb_conv1d_step.restype = ctypes.c_int
     lib.mb_conv1d_step.argtypes = [ctypes.c_int64] * 2 + [ctypes.c_int32] * 4 + [_VP] * 6
     lib.mb_scan_bwd.restype = ctypes.c_int
-    lib.mb_scan_bwd.argtypes = [ctypes.POINTER(ScanDesc)] + [_VP] * 21
+    lib.mb_scan_bwd.argtypes = [ctypes.POINTER(ScanDesc)] + [_VP] * 22
+    lib.mb_scan_fwd_ckpt.restype = ctypes.c_int
+    lib.mb_scan_fwd_ckpt.argtypes = [ctypes.POINTER(ScanDesc)] + [_VP] * 13
     lib.mb_verify_rank.restype = ctypes.c_int
     lib.mb_verify_rank.argtypes = [ctypes.c_int64] * 3 + [ctypes.c_int32] * 2 + [_VP] * 6
     lib.mb_status_string.restype = ctypes.c_char_p
@@ -105,7 +107,7 @@ def _need(t, name, shape, dtype=None, device=None):
 
 def scan_fwd(u, delta, A, B, C, D=None, dt_bias=None, z=None, h0=None, *, delta_softplus=True,
              out_dtype=torch.float32, return_last_state=False, out=None, h_last=None,
-             positions=None, h_at=None):
+             positions=None, h_at=None, return_ckpt=False, ck=None):
     """Selective scan over (batch, dim, L) inputs; returns y or (y, h_last).
 
     u, delta, z: (batch, dim, L); B, C: (batch, N, L), all of one dtype (fp32 or bf16);
@@ -115,6 +117,10 @@ def scan_fwd(u, delta, A, B, C, D=None, dt_bias=None, z=None, h0=None, *, delta_
     timestep in [0, L) or -1 (the initial state).  The states there are returned as a
     last extra element ``h_at`` of shape (npos, batch, dim, N) (NaN for a position
     outside [-1, L-1]); ``h_at[k]`` can be passed back as ``h0`` to resume.
+
+    ``return_ckpt`` (or a given ``ck``): also store the backward's checkpoints, the
+    state before every 16th timestep, as a last extra element of shape
+    (L // 16, batch, dim, N) (mb_scan_fwd_ckpt; not combined with positions).
     """
     lib = load_library()
     if not isinstance(u, torch.Tensor) or u.dim() != 3:
@@ -157,10 +163,22 @@ def scan_fwd(u, delta, A, B, C, D=None, dt_bias=None, z=None, h0=None, *, delta_
             _need(h_at, "h_at", (npos, nb, dim, N), torch.float32, dev)
     elif h_at is not None:
         raise MBScanError("h_at given without positions")
+    want_ck = return_ckpt or ck is not None
+    if want_ck:
+        if positions is not None:
+            raise MBScanError("checkpoints and positions are not recorded by the same call")
+        if ck is None:
+            ck = torch.empty((L // 16, nb, dim, N), dtype=torch.float32, device=dev)
+        else:
+            _need(ck, "ck", (L // 16, nb, dim, N), torch.float32, dev)
     desc = ScanDesc(nb, dim, L, N, _dt(act), _dt(out.dtype), 1 if delta_softplus else 0, 0)
     stream = torch.cuda.current_stream(dev).cuda_stream
     with torch.cuda.device(dev):
-        if positions is None:
+        if want_ck:
+            st = lib.mb_scan_fwd_ckpt(ctypes.byref(desc), _ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C),
+                                      _ptr(D), _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(out), _ptr(h_last),
+                                      _ptr(ck), stream)
+        elif positions is None:
             st = lib.mb_scan_fwd(ctypes.byref(desc), _ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C),
                                  _ptr(D), _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(out), _ptr(h_last),
                                  stream)
@@ -168,12 +186,14 @@ def scan_fwd(u, delta, A, B, C, D=None, dt_bias=None, z=None, h0=None, *, delta_
             st = lib.mb_scan_fwd_states(ctypes.byref(desc), _ptr(u), _ptr(delta), _ptr(A), _ptr(B),
                                         _ptr(C), _ptr(D), _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(out),
                                         _ptr(h_last), _ptr(positions), npos, _ptr(h_at), stream)
-    _check(st, "mb_scan_fwd" if positions is None else "mb_scan_fwd_states")
+    _check(st, "mb_scan_fwd_ckpt" if want_ck else "mb_scan_fwd" if positions is None else "mb_scan_fwd_states")
     res = (out,)
     if return_last_state or h_last is not None:
         res += (h_last,)
     if positions is not None:
         res += (h_at,)
+    if want_ck:
+        res += (ck,)
     return res[0] if len(res) == 1 else res
 
 
@@ -301,8 +321,11 @@ def verify_rank(logits, draft, beta, *, return_ranks=False):
 
 
 def scan_bwd(u, delta, A, B, C, dy, D=None, dt_bias=None, z=None, h0=None, dh_last=None, *,
-             delta_softplus=True):
+             delta_softplus=True, ck=None):
     """Gradients of sum(dy * y) + sum(dh_last * h_last) for the scan of scan_fwd.
+
+    ``ck``: the checkpoints of ``scan_fwd(..., return_ckpt=True)`` on the same inputs;
+    without them the call recomputes them with one more forward pass.
 
     dy has y's dtype (fp32 or bf16), shape (batch, dim, L).  Returns a dict: du, ddelta,
     dz (dy's dtype, (batch, dim, L); dz None without a gate), dA (dim, N), dB, dC
@@ -324,7 +347,8 @@ def scan_bwd(u, delta, A, B, C, dy, D=None, dt_bias=None, z=None, h0=None, dh_la
     for t, name, shape, dt in ((z, "z", (nb, dim, L), act), (D, "D", (dim,), torch.float32),
                                (dt_bias, "dt_bias", (dim,), torch.float32),
                                (h0, "h0", (nb, dim, N), torch.float32),
-                               (dh_last, "dh_last", (nb, dim, N), torch.float32)):
+                               (dh_last, "dh_last", (nb, dim, N), torch.float32),
+                               (ck, "ck", (L // 16, nb, dim, N), torch.float32)):
         if t is not None:
             _need(t, name, shape, dt, dev)
     f32 = dict(dtype=torch.float32, device=dev)
@@ -340,7 +364,8 @@ def scan_bwd(u, delta, A, B, C, dy, D=None, dt_bias=None, z=None, h0=None, dh_la
     stream = torch.cuda.current_stream(dev).cuda_stream
     with torch.cuda.device(dev):
         st = lib.mb_scan_bwd(ctypes.byref(desc), _ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C), _ptr(D),
-                             _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(dy), _ptr(dh_last), _ptr(g["du"]),
+                             _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(dy), _ptr(dh_last), _ptr(ck),
+                             _ptr(g["du"]),
                              _ptr(g["ddelta"]), _ptr(g["dz"]), _ptr(g["dA"]), _ptr(g["dB"]), _ptr(g["dC"]),
                              _ptr(g["dD"]), _ptr(g["ddt_bias"]), _ptr(g["dh0"]), stream)
     _check(st, "mb_scan_bwd")

@@ -161,16 +161,17 @@ hipError_t zero_async(float *p, int64_t n, hipStream_t st) {
 }
 
 template <int IN, int OUT, bool GATE, bool SP>
-hipError_t bwd_launch(mbs::bwd::BwdParams &p, float *dA, float *dB, float *dC, float *dD, float *dbias,
-                      hipStream_t st) {
+hipError_t bwd_launch(mbs::bwd::BwdParams &p, bool have_ck, float *dA, float *dB, float *dC, float *dD,
+                      float *dbias, hipStream_t st) {
     namespace W = mbs::bwd;
     const int64_t n_cg = (p.dim + W::kCh - 1) / W::kCh;
     const int64_t waves = n_cg * p.batch;
     const dim3 grid((unsigned)((waves + W::kWaves - 1) / W::kWaves)), block(W::kThreads);
     const size_t lds = sizeof(W::WaveSmem) * W::kWaves;
     void *args[] = {&p};
-    hipError_t e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_ckpt<IN, SP>), grid, block, args, lds,
-                                   st);
+    hipError_t e = hipSuccess;
+    if (!have_ck)
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_ckpt<IN, SP>), grid, block, args, lds, st);
     if (e != hipSuccess) return e;
     e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_bwd<IN, OUT, GATE, SP>), grid, block, args, lds,
                         st);
@@ -188,13 +189,13 @@ hipError_t bwd_launch(mbs::bwd::BwdParams &p, float *dA, float *dB, float *dC, f
 }
 
 template <int IN, int OUT>
-hipError_t bwd_dispatch(mbs::bwd::BwdParams &p, float *dA, float *dB, float *dC, float *dD, float *dbias,
-                        hipStream_t st) {
+hipError_t bwd_dispatch(mbs::bwd::BwdParams &p, bool have_ck, float *dA, float *dB, float *dC, float *dD,
+                        float *dbias, hipStream_t st) {
     if (p.z)
-        return p.delta_softplus ? bwd_launch<IN, OUT, true, true>(p, dA, dB, dC, dD, dbias, st)
-                                : bwd_launch<IN, OUT, true, false>(p, dA, dB, dC, dD, dbias, st);
-    return p.delta_softplus ? bwd_launch<IN, OUT, false, true>(p, dA, dB, dC, dD, dbias, st)
-                            : bwd_launch<IN, OUT, false, false>(p, dA, dB, dC, dD, dbias, st);
+        return p.delta_softplus ? bwd_launch<IN, OUT, true, true>(p, have_ck, dA, dB, dC, dD, dbias, st)
+                                : bwd_launch<IN, OUT, true, false>(p, have_ck, dA, dB, dC, dD, dbias, st);
+    return p.delta_softplus ? bwd_launch<IN, OUT, false, true>(p, have_ck, dA, dB, dC, dD, dbias, st)
+                            : bwd_launch<IN, OUT, false, false>(p, have_ck, dA, dB, dC, dD, dbias, st);
 }
 
 }  // namespace
@@ -217,17 +218,15 @@ const char *mb_status_string(int status) {
     }
 }
 
-int mb_scan_fwd(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
-                const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
-                const void *z, const float *h0, void *y, float *h_last, void *stream) {
-    return mb_scan_fwd_states(desc, u, delta, A, Bmat, Cmat, Dskip, dt_bias, z, h0, y, h_last, nullptr, 0,
-                              nullptr, stream);
-}
+}  // extern "C"
 
-int mb_scan_fwd_states(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
-                       const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
-                       const void *z, const float *h0, void *y, float *h_last, const int32_t *pos,
-                       int64_t npos, float *h_pos, void *stream) {
+namespace {
+
+// The forward scan behind mb_scan_fwd, mb_scan_fwd_states and mb_scan_fwd_ckpt.
+int scan_fwd_impl(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
+                  const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
+                  const void *z, const float *h0, void *y, float *h_last, const int32_t *pos,
+                  int64_t npos, float *h_pos, float *ck, void *stream) {
     if (!desc) return MB_ERR_NULL;
     const int64_t B = desc->batch, D = desc->dim, L = desc->seqlen, N = desc->dstate;
     if (B < 0 || D < 0 || L < 0 || N < 0) return MB_ERR_SHAPE;
@@ -286,7 +285,24 @@ int mb_scan_fwd_states(const mb_scan_desc *desc, const void *u, const void *delt
     p.A = A; p.Dskip = Dskip; p.dt_bias = dt_bias; p.h0 = h0;
     p.y = y; p.h_last = h_last;
     p.pos = npos > 0 ? pos : nullptr; p.npos = npos; p.h_pos = npos > 0 ? h_pos : nullptr;
+    p.ck = nullptr;
     p.delta_softplus = desc->delta_softplus ? 1 : 0;
+
+    if (ck) {
+        // checkpoints exist on the tiled path only: dstate 16, L a multiple of 16,
+        // 16-byte aligned activations and y
+        if (N != 16 || L % 16 != 0 || L >= (int64_t(1) << 25)) return MB_ERR_UNSUPPORTED;
+        const void *a16[] = {u, delta, z, Bmat, Cmat, y};
+        for (const void *q : a16)
+            if (q && !aligned(q, 16)) return MB_ERR_ALIGN;
+        if (!aligned(ck, 8)) return MB_ERR_ALIGN;
+        const size_t ck_bytes = (size_t)elems * 4;        // (L / 16) x rows x 16 floats
+        for (const Range &r : ins)
+            if (overlaps(ck, ck_bytes, r.p, r.n)) return MB_ERR_ALIAS;
+        if (overlaps(ck, ck_bytes, y, y_bytes) || overlaps(ck, ck_bytes, h_last, st_bytes)) return MB_ERR_ALIAS;
+        if (L > 0 && !tiled_ok(p, N, desc->in_dtype, desc->out_dtype)) return MB_ERR_UNSUPPORTED;
+        p.ck = ck;
+    }
 
     if (npos > 0) {
         // Position -1 and invalid positions, before h_last (which may be h0) is written.
@@ -314,6 +330,33 @@ int mb_scan_fwd_states(const mb_scan_desc *desc, const void *u, const void *delt
     else
         e = desc->out_dtype == MB_F32 ? fwd_dispatch_n<1, 0>(p, N, stream) : fwd_dispatch_n<1, 1>(p, N, stream);
     return e == hipSuccess ? MB_OK : MB_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mb_scan_fwd(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
+                const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
+                const void *z, const float *h0, void *y, float *h_last, void *stream) {
+    return scan_fwd_impl(desc, u, delta, A, Bmat, Cmat, Dskip, dt_bias, z, h0, y, h_last, nullptr, 0, nullptr,
+                         nullptr, stream);
+}
+
+int mb_scan_fwd_states(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
+                       const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
+                       const void *z, const float *h0, void *y, float *h_last, const int32_t *pos,
+                       int64_t npos, float *h_pos, void *stream) {
+    return scan_fwd_impl(desc, u, delta, A, Bmat, Cmat, Dskip, dt_bias, z, h0, y, h_last, pos, npos, h_pos,
+                         nullptr, stream);
+}
+
+int mb_scan_fwd_ckpt(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
+                     const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
+                     const void *z, const float *h0, void *y, float *h_last, float *ck, void *stream) {
+    if (!ck) return MB_ERR_NULL;
+    return scan_fwd_impl(desc, u, delta, A, Bmat, Cmat, Dskip, dt_bias, z, h0, y, h_last, nullptr, 0, nullptr,
+                         ck, stream);
 }
 
 int mb_conv1d_fwd(const mb_conv_desc *desc, const void *x, const float *w, const float *bias,
@@ -398,7 +441,7 @@ int mb_conv1d_step(int64_t batch, int64_t dim, int32_t width, int32_t in_dtype, 
 
 int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
                 const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
-                const void *z, const float *h0, const void *dy, const float *dh_last,
+                const void *z, const float *h0, const void *dy, const float *dh_last, const float *ck,
                 void *du, void *ddelta, void *dz, float *dA, float *dB, float *dC, float *dDskip,
                 float *ddt_bias, float *dh0, void *stream) {
     if (!desc) return MB_ERR_NULL;
@@ -422,7 +465,7 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     const void *act_out[] = {dy, du, ddelta, dz};
     for (const void *q : act_out)
         if (q && !aligned(q, 16)) return MB_ERR_ALIGN;
-    const void *f32s[] = {A, Dskip, dt_bias, h0, dh_last, dA, dB, dC, dDskip, ddt_bias, dh0};
+    const void *f32s[] = {A, Dskip, dt_bias, h0, dh_last, ck, dA, dB, dC, dDskip, ddt_bias, dh0};
     for (const void *q : f32s)
         if (q && !aligned(q, 8)) return MB_ERR_ALIGN;
     // outputs overlap nothing
@@ -430,7 +473,8 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     const size_t st_b = (size_t)state_elems * 4, a_b = (size_t)(D * N) * 4, v_b = (size_t)D * 4;
     struct Range { const void *p; size_t n; };
     const Range ins[] = {{u, in_b}, {delta, in_b}, {z, in_b}, {Bmat, bc_b}, {Cmat, bc_b}, {A, a_b},
-                         {Dskip, v_b}, {dt_bias, v_b}, {h0, st_b}, {dy, out_b}, {dh_last, st_b}};
+                         {Dskip, v_b}, {dt_bias, v_b}, {h0, st_b}, {dy, out_b}, {dh_last, st_b},
+                         {ck, (size_t)elems * 4}};
     const Range outs[] = {{du, out_b}, {ddelta, out_b}, {dz, z ? out_b : 0}, {dA, a_b},
                           {dB, (size_t)bc_elems * 4}, {dC, (size_t)bc_elems * 4}, {dDskip, v_b},
                           {ddt_bias, v_b}, {dh0, st_b}};
@@ -459,7 +503,7 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
 
     namespace W = mbs::bwd;
     const int64_t n_cg = (D + W::kCh - 1) / W::kCh;
-    const size_t ck_b = (size_t)(L / W::kT) * (size_t)rows * W::kN * 4;
+    const size_t ck_b = ck ? 0 : (size_t)(L / W::kT) * (size_t)rows * W::kN * 4;
     const size_t bcp_b = (size_t)n_cg * (size_t)B * (size_t)L * W::kQ * 4 * 4;
     const size_t row_b = (size_t)rows * (W::kN + 2) * 4;
     char *ws = nullptr;
@@ -471,17 +515,17 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     p.A = A; p.Dskip = Dskip; p.dt_bias = dt_bias; p.h0 = h0;
     p.dy = dy; p.dh_last = dh_last;
     p.du = du; p.ddelta = ddelta; p.dz = dz; p.dh0 = dh0;
-    p.ck = reinterpret_cast<float *>(ws);
+    p.ck = ck ? const_cast<float *>(ck) : reinterpret_cast<float *>(ws);   // given: read only
     p.part_bc = reinterpret_cast<float *>(ws + ck_b);
     p.part_row = reinterpret_cast<float *>(ws + ck_b + bcp_b);
     p.delta_softplus = desc->delta_softplus ? 1 : 0;
     float *dD = Dskip ? dDskip : nullptr, *dbias = dt_bias ? ddt_bias : nullptr;
     if (desc->in_dtype == MB_F32)
-        e = desc->out_dtype == MB_F32 ? bwd_dispatch<0, 0>(p, dA, dB, dC, dD, dbias, st)
-                                      : bwd_dispatch<0, 1>(p, dA, dB, dC, dD, dbias, st);
+        e = desc->out_dtype == MB_F32 ? bwd_dispatch<0, 0>(p, ck != nullptr, dA, dB, dC, dD, dbias, st)
+                                      : bwd_dispatch<0, 1>(p, ck != nullptr, dA, dB, dC, dD, dbias, st);
     else
-        e = desc->out_dtype == MB_F32 ? bwd_dispatch<1, 0>(p, dA, dB, dC, dD, dbias, st)
-                                      : bwd_dispatch<1, 1>(p, dA, dB, dC, dD, dbias, st);
+        e = desc->out_dtype == MB_F32 ? bwd_dispatch<1, 0>(p, ck != nullptr, dA, dB, dC, dD, dbias, st)
+                                      : bwd_dispatch<1, 1>(p, ck != nullptr, dA, dB, dC, dD, dbias, st);
     const hipError_t f = hipFreeAsync(ws, st);
     if (e == hipSuccess) e = f;
     return e == hipSuccess ? MB_OK : MB_ERR_HIP;

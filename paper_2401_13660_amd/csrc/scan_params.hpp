@@ -18,6 +18,10 @@ struct ScanParams {
     const int32_t *pos;
     int64_t npos;
     float *h_pos;
+    // Checkpoints for the backward (tiled path only): ck[((t / 16) * batch * dim
+    // + row) * 16 + n] receives the state before timestep t for every t that is a
+    // multiple of 16 (h0 at t = 0).  Null disables them.
+    float *ck;
     int delta_softplus;
 };
 

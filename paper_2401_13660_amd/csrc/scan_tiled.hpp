@@ -88,7 +88,9 @@ struct WaveSmem {
 //   Folding h <- P h + H is the associative operator of the parallel-scan
 //   formulation (Section 2, "Implementation") applied across segments.
 // POS = true (scan only): also record the states at p.pos (p.npos > 0).
-template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool PREPASS, bool POS>
+// CK = true (scan only): also store the state at every 16-timestep boundary in
+//   p.ck, the checkpoints the backward recomputes its chunks from.
+template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool PREPASS, bool POS, bool CK = false>
 __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len, float *carry) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -241,6 +243,14 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         }
     };
 
+    auto store_ck = [&](int64_t t) {                 // the state before timestep t
+        if (live) {
+            float *c = p.ck + ((t / 16) * rows + row) * kN + n0;
+            c[0] = h[0];
+            c[1] = h[1];
+        }
+    };
+
     auto chunk = [&](Slot &sl, int64_t t0) {
         const int nt = (int)(t_end - t0 < kT ? t_end - t0 : kT);   // valid timesteps, multiple of 16
 
@@ -273,6 +283,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         //      step i + 1 are read from LDS while step i computes ----------------
         const float hs0 = POS ? h[0] : 0.0f;        // the state before this chunk
         const float hs1 = POS ? h[1] : 0.0f;
+        if (CK) store_ck(t0);
         {
             f32x4 ddA[2], bcA[4], ddB[2], bcB[4];
             using I0 = std::integral_constant<int, 0>;
@@ -293,6 +304,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
             if (nt == kT) {
                 load4(ddA, bcA, I4{});
                 recur4(ddB, bcB, I3{});
+                if (CK) store_ck(t0 + 16);
                 load4(ddB, bcB, I5{});
                 recur4(ddA, bcA, I4{});
                 load4(ddA, bcA, I6{});
@@ -404,9 +416,10 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
     const int64_t waves = n_cg * p.batch * nseg;
     const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;
     void *args[] = {&p, &seg_len, &carry};
-    const void *main_fn = p.npos > 0
-        ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, true>)
-        : reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false>);
+    const void *main_fn =
+        p.npos > 0 ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, true>)
+        : p.ck     ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false, true>)
+                   : reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false>);
     e = hipLaunchKernel(main_fn, dim3((unsigned)blocks), dim3(kThreads), args, lds, st);
     if (carry) {
         const hipError_t f = hipFreeAsync(carry, st);

@@ -31,14 +31,15 @@ def test_exports_every_declared_symbol():
     lib = mb.load_library()
     names = declared_functions()
     assert {"mb_scan_fwd", "mb_scan_fwd_states", "mb_scan_step", "mb_conv1d_fwd", "mb_conv1d_step",
-            "mb_verify_rank", "mb_scan_bwd", "mb_status_string", "mb_abi_version"} <= set(names)
+            "mb_verify_rank", "mb_scan_bwd", "mb_scan_fwd_ckpt", "mb_status_string",
+            "mb_abi_version"} <= set(names)
     for n in names:
         assert hasattr(lib, n), f"{n} declared in mbscan.h but not exported"
 
 
 def test_version_and_status_strings():
     lib = mb.load_library()
-    assert lib.mb_abi_version() == 5
+    assert lib.mb_abi_version() == 6
     for code in range(-7, 1):
         assert lib.mb_status_string(code)
     assert lib.mb_status_string(-99) == b"unknown status"
@@ -116,6 +117,70 @@ def _fwd_states(desc, npos, **over):
 ])
 def test_fwd_states_rejects(npos, over, code):
     assert _fwd_states(_desc(), npos, **over) == code
+
+
+CK = 0x0a000000
+
+
+def _fwd_ckpt(desc, **over):
+    a = dict(P, ck=CK)
+    a.update(over)
+    lib = mb.load_library()
+    return lib.mb_scan_fwd_ckpt(ctypes.byref(desc), a["u"], a["delta"], a["A"], a["B"], a["C"], a["D"],
+                                a["bias"], a["z"], a["h0"], a["y"], a["hl"], a["ck"], None)
+
+
+@no_gpu_only
+@pytest.mark.parametrize("desc,over,code", [
+    (_desc(), dict(ck=None), -1),
+    (_desc(dstate=8), {}, -5),                          # checkpoints exist for dstate 16 only
+    (_desc(seqlen=24), {}, -5),                         # and L a multiple of 16
+    (_desc(), dict(u=P["u"] + 2), -4),                  # activations 16-byte aligned
+    (_desc(), dict(y=P["y"] + 8), -4),
+    (_desc(), dict(ck=CK + 4), -4),
+    (_desc(), dict(ck=P["u"] + 16), -7),                # checkpoints inside u
+    (_desc(), dict(ck=P["y"]), -7),                     # on top of y
+    (_desc(), dict(ck=P["hl"] - 64), -7),               # running into h_last
+    (_desc(), dict(A=None), -1),                        # the mb_scan_fwd checks still apply
+])
+def test_fwd_ckpt_rejects(desc, over, code):
+    assert _fwd_ckpt(desc, **over) == code
+
+
+BP = {k: 0x30000000 + 0x01000000 * i for i, k in enumerate(
+    ["u", "delta", "A", "B", "C", "D", "bias", "z", "h0", "dy", "dhl", "ck", "du", "ddelta", "dz", "dA", "dB",
+     "dC", "dD", "dbias", "dh0"])}
+
+
+def _bwd(desc, **over):
+    a = dict(BP)
+    a.update(over)
+    lib = mb.load_library()
+    order = ["u", "delta", "A", "B", "C", "D", "bias", "z", "h0", "dy", "dhl", "ck", "du", "ddelta", "dz", "dA",
+             "dB", "dC", "dD", "dbias", "dh0"]
+    return lib.mb_scan_bwd(ctypes.byref(desc) if desc is not None else None, *[a[k] for k in order], None)
+
+
+@no_gpu_only
+@pytest.mark.parametrize("desc,over,code", [
+    (None, {}, -1),
+    (_desc(batch=-1), {}, -2),
+    (_desc(in_dtype=9), {}, -3),
+    (_desc(dstate=8), {}, -5),
+    (_desc(seqlen=24), {}, -5),
+    (_desc(reserved=1), {}, -5),
+    (_desc(), dict(dy=None), -1),
+    (_desc(), dict(dA=None), -1),
+    (_desc(), dict(dz=None), -1),                       # z given, dz missing
+    (_desc(), dict(dD=None), -1),                       # Dskip given, its gradient missing
+    (_desc(), dict(du=BP["du"] + 4), -4),               # activations and gradients 16-byte aligned
+    (_desc(), dict(ck=BP["ck"] + 4), -4),
+    (_desc(), dict(du=BP["u"] + 32), -7),               # an output inside an input
+    (_desc(), dict(dB=BP["ck"]), -7),                   # an output on the checkpoints
+    (_desc(), dict(dC=BP["dB"] + 64), -7),              # two outputs overlapping
+])
+def test_bwd_rejects(desc, over, code):
+    assert _bwd(desc, **over) == code
 
 
 def _cdesc(**kw):

@@ -118,3 +118,65 @@ def test_bwd_972m_layer_sampled_rows():
     rows = np.sort(np.random.default_rng(66).choice(inp.batch * inp.dim, 32, replace=False))
     announce("bwd 972M layer (4, 3584, 8192)")
     grads_case(inp, with_dhl=False, rows=rows)
+
+
+# ---- the training pair: the forward stores the checkpoints, the backward reads them
+
+def _fwd_ckpt(t):
+    import paper_2401_13660_amd as mb
+    kw = dict(D=t.get("Dskip"), dt_bias=t.get("dt_bias"), z=t.get("z"), h0=t.get("h0"), return_last_state=True)
+    y, hl, ck = mb.scan_fwd(t["u"], t["delta"], t["A"], t["B"], t["C"], return_ckpt=True, **kw)
+    y0, hl0 = mb.scan_fwd(t["u"], t["delta"], t["A"], t["B"], t["C"], **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y0), "storing checkpoints changed y"
+    assert torch.equal(hl, hl0), "storing checkpoints changed h_last"
+    return ck
+
+
+# (batch, dim, L): whole 32-step chunks with dead lanes; a trailing half chunk;
+# one row group cut into time segments (the forward's pre-pass path).
+@pytest.mark.parametrize("shape", [(2, 196, 512), (3, 100, 208), (1, 64, 1024)])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_fwd_checkpoints_match_oracle_states(shape, dtype):
+    """ck[k] is the state before timestep 16k: the oracle's state at position 16k - 1."""
+    nb, dim, L = shape
+    inp = make_inputs(nb, dim, L, 16, dtype=dtype, seed=67, with_h0=True)
+    announce(f"forward checkpoints {shape} {dtype}")
+    ck = _fwd_ckpt({k: dev_tensor(v) for k, v in inp.arrays().items()})
+    pos = np.repeat((np.arange(L // 16) * 16 - 1)[:, None], nb, axis=1).astype(np.int32)
+    _, _, h_ref = oracle.scan_inputs(inp, positions=pos)                  # (L/16, rows, N)
+    got = ck.cpu().numpy().reshape(L // 16, nb * dim, 16).astype(np.float64)
+    assert np.array_equal(got[0], inp.h0.reshape(nb * dim, 16).astype(np.float64)), "ck[0] is not h0"
+    e = rel_err(got, h_ref)
+    print(f"[ck error] {e:.2e}", flush=True)
+    assert e <= 1e-4, f"checkpoints: relative error {e:.3e}"
+
+
+@pytest.mark.parametrize("shape,gated", [((2, 196, 512), True), ((1, 64, 1024), False)])
+def test_bwd_from_forward_checkpoints(shape, gated):
+    """The backward from the forward's checkpoints: oracle parity, and the same
+    gradients as the backward that recomputes its checkpoints."""
+    import paper_2401_13660_amd as mb
+    inp = make_inputs(*shape, 16, dtype="bf16", seed=68, with_h0=True, gated=gated)
+    announce(f"bwd from forward checkpoints {shape} gated={gated}")
+    t = {k: dev_tensor(v) for k, v in inp.arrays().items()}
+    ck = _fwd_ckpt(t)
+    dy = torch.randn(inp.u.shape, generator=torch.Generator().manual_seed(3)).to("cuda:0")
+    kw = dict(D=t.get("Dskip"), dt_bias=t.get("dt_bias"), z=t.get("z"), h0=t.get("h0"))
+    g_ck = mb.scan_bwd(t["u"], t["delta"], t["A"], t["B"], t["C"], dy, ck=ck, **kw)
+    g_re = mb.scan_bwd(t["u"], t["delta"], t["A"], t["B"], t["C"], dy, **kw)
+    torch.cuda.synchronize()
+    same = all(torch.equal(g_ck[k], g_re[k]) for k in g_ck if g_ck[k] is not None)
+    print(f"[bwd from ck] bit-identical to the recomputing call: {same}", flush=True)
+    for k in g_ck:
+        if g_ck[k] is None:
+            continue
+        e = rel_err(g_ck[k].double().cpu().numpy(), g_re[k].double().cpu().numpy())
+        assert e <= 1e-5, f"{k}: {e:.3e} between the two checkpoint sources"
+    ref = oracle.default().scan_bwd(inp.u, inp.delta, inp.A, inp.B, inp.C, dy.cpu().numpy(), z=inp.z,
+                                    Dskip=inp.Dskip, dt_bias=inp.dt_bias, h0=inp.h0, dtype=inp.dtype)
+    for k in g_ck:
+        if g_ck[k] is None:
+            continue
+        e = rel_err(g_ck[k].double().cpu().numpy(), ref[ORACLE_NAME[k]])
+        assert e <= TOL[k], f"{k}: relative error {e:.3e} > {TOL[k]:.1e}"
