@@ -54,7 +54,8 @@ struct BwdParams {
     float *dh0;                        // (batch, dim, N) or null
     // workspace
     float *ck;                         // (L / 16, batch * dim, 16) checkpoints
-    float *part_bc;                    // (ncg, batch, L, 8, 4): per wave, summed over its channels
+    float *part_bc;                    // (ncg, batch, L, 8, 4): per wave, summed over its channels:
+                                       // (dB[2q], dC[2q], dB[2q+1], dC[2q+1]) of state pair q
     float *part_row;                   // (batch * dim, 16 + 2): dA (16), dDskip, dbias per row
     int delta_softplus;
 };
@@ -109,15 +110,26 @@ __device__ __forceinline__ void wave_sync() {
 __device__ __forceinline__ void part_sum(const f32x4 (&part)[kCh * (kT / 4)][kQ + 1], int j, int q,
                                          float (&out)[2]) {
     const float *base = reinterpret_cast<const float *>(&part[4 * j + (q >> 1)][0]) + 2 * (q & 1);
-    float s0 = 0.0f, s1 = 0.0f;
+    const float2 v0 = *reinterpret_cast<const float2 *>(base);
+    float s0 = v0.x, s1 = v0.y;
 #pragma unroll
-    for (int w = 0; w < kQ; ++w) {
+    for (int w = 1; w < kQ; ++w) {
         const float2 v = *reinterpret_cast<const float2 *>(base + 4 * w);
         s0 += v.x;
         s1 += v.y;
     }
     out[0] = s0;
     out[1] = s1;
+}
+
+// Sums over lanes l and l + 32 of two values at once: lanes 0-31 receive a's,
+// lanes 32-63 b's (v_permlane32_swap exchanges lanes 32-63 of its first
+// operand with lanes 0-31 of its second).  The halves are copied to scalars
+// before reinterpreting them.
+__device__ __forceinline__ float half_swap_sum(float a, float b) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+    const unsigned r0 = r[0], r1 = r[1];
+    return __uint_as_float(r0) + __uint_as_float(r1);
 }
 
 // The wave's (batch, channel group) from a workgroup renumbered so that each of
@@ -289,9 +301,9 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
                     ab[t][s] = hw_exp2(dv.x * a2[s]);
                     hb[t + 1][s] = __builtin_fmaf(ab[t][s], hb[t][s], dv.y * bv[s]);
                 }
-                acc[k] = __builtin_fmaf(bv.w, hb[t + 1][1], bv.z * hb[t + 1][0]);
+                if (GATE) acc[k] = __builtin_fmaf(bv.w, hb[t + 1][1], bv.z * hb[t + 1][0]);
             }
-            sm.pa[4 * j + tq][q] = f32x4{acc[0], acc[1], acc[2], acc[3]};
+            if (GATE) sm.pa[4 * j + tq][q] = f32x4{acc[0], acc[1], acc[2], acc[3]};   // C . h, for dz
         }
         wave_sync();
 
@@ -335,17 +347,18 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
             sm.pb[4 * j + tq][q] = f32x4{pd[0], pd[1], pd[2], pd[3]};
             wave_sync();
             // dB / dC of timesteps 4tq .. 4tq+3 summed over the wave's 8 channels:
-            // lane (half, k, q') sums channels 4 half .. 4 half + 3, the halves meet
-            // through a lane exchange, and half 0 writes 16 bytes of the partial.
+            // lane (half, k, q') sums channels 4 half .. 4 half + 3; the halves meet
+            // in a swap that leaves state 2q' (dB, dC) in half 0 and state 2q'+1 in
+            // half 1, and every lane writes its 8 bytes of the partial.
             {
                 const int half = lane >> 5, kk = (lane >> 3) & 3, qq = lane & 7;
                 f32x4 sum = sm.x[kk][qq][4 * half];
 #pragma unroll
                 for (int i = 1; i < 4; ++i) sum += sm.x[kk][qq][4 * half + i];
-#pragma unroll
-                for (int c = 0; c < 4; ++c) sum[c] += __shfl_xor(sum[c], 32, 64);
-                if (half == 0)
-                    *reinterpret_cast<f32x4 *>(pbc + ((t0 + 4 * tq + kk) * kQ + qq) * 4) = sum;
+                const float db = half_swap_sum(sum.x, sum.y);   // dB[2q'] | dB[2q'+1]
+                const float dc = half_swap_sum(sum.z, sum.w);   // dC[2q'] | dC[2q'+1]
+                *reinterpret_cast<float2 *>(pbc + ((t0 + 4 * tq + kk) * kQ + qq) * 4 + 2 * half) =
+                    make_float2(db, dc);
             }
             wave_sync();                                // x is rewritten by the next step
         }
@@ -413,8 +426,8 @@ __global__ __launch_bounds__(256) void bwd_finish_bc(BwdParams p, float *dB, flo
     for (int64_t c = 0; c < ncg; ++c) sum += *reinterpret_cast<const f32x4 *>(src + c * stride);
     const int64_t n0 = 2 * qq;
     dB[(b * kN + n0) * L + t] = sum.x;
-    dB[(b * kN + n0 + 1) * L + t] = sum.y;
-    dC[(b * kN + n0) * L + t] = sum.z;
+    dC[(b * kN + n0) * L + t] = sum.y;
+    dB[(b * kN + n0 + 1) * L + t] = sum.z;
     dC[(b * kN + n0 + 1) * L + t] = sum.w;
 }
 
