@@ -291,11 +291,17 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
 #pragma unroll
         for (int tq = 0; tq < kT / 4; ++tq) {
             float acc[4];
+            f32x4 dvs[4], bvs[4];                       // the 4 steps' operands, read together
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                dvs[k] = sm.dd[4 * tq + k][j];
+                bvs[k] = sm.bc[4 * tq + k][q];
+            }
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const int t = 4 * tq + k;
-                const f32x4 dv = sm.dd[t][j];
-                const f32x4 bv = sm.bc[t][q];
+                const f32x4 dv = dvs[k];
+                const f32x4 bv = bvs[k];
 #pragma unroll
                 for (int s = 0; s < 2; ++s) {
                     ab[t][s] = hw_exp2(dv.x * a2[s]);
@@ -325,11 +331,17 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
 #pragma unroll
         for (int tq = kT / 4 - 1; tq >= 0; --tq) {
             float pu[4], pd[4];
+            f32x4 dvs[4], bvs[4];                       // the 4 steps' operands, read together
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                dvs[k] = sm.dd[4 * tq + k][j];
+                bvs[k] = sm.bc[4 * tq + k][q];
+            }
 #pragma unroll
             for (int k = 3; k >= 0; --k) {
                 const int t = 4 * tq + k;
-                const f32x4 dv = sm.dd[t][j];          // (dlt, dlt*u, ds, u)
-                const f32x4 bv = sm.bc[t][q];          // (B0, B1, C0, C1)
+                const f32x4 dv = dvs[k];               // (dlt, dlt*u, ds, u)
+                const f32x4 bv = bvs[k];               // (B0, B1, C0, C1)
                 const float lam0 = __builtin_fmaf(dv.z, bv.z, carry[0]);
                 const float lam1 = __builtin_fmaf(dv.z, bv.w, carry[1]);
                 sm.x[k][q][j] = f32x4{lam0 * dv.y, lam1 * dv.y, dv.z * hb[t + 1][0], dv.z * hb[t + 1][1]};
