@@ -98,6 +98,11 @@ struct WaveSmem {
     f32x4 x[4][kQ][kCh + 1];          // dB / dC contributions of 4 timesteps, summed over j
 };
 
+// The first two words of a 16-byte LDS entry, as one 8-byte read.  (Reading the
+// whole entry when two words are used lets the compiler reuse the unused half of
+// the destination for the next read, which then has to wait for this one.)
+__device__ __forceinline__ float2 lo2(const f32x4 &e) { return *reinterpret_cast<const float2 *>(&e); }
+
 __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -190,11 +195,18 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
                 u32x2{__builtin_bit_cast(uint32_t, h[0]), __builtin_bit_cast(uint32_t, h[1])};
         wave_sync();
 #pragma unroll
-        for (int t = 0; t < kT; ++t) {
-            const f32x4 dv = sm.dd[t][j];
-            const f32x4 bv = sm.bc[t][q];
-            h[0] = __builtin_fmaf(hw_exp2(dv.x * a2[0]), h[0], dv.y * bv.x);
-            h[1] = __builtin_fmaf(hw_exp2(dv.x * a2[1]), h[1], dv.y * bv.y);
+        for (int tq = 0; tq < kT / 4; ++tq) {
+            float2 dvs[4], bvs[4];                      // (dlt, dlt*u), (B0, B1) of 4 steps, read together
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                dvs[k] = lo2(sm.dd[4 * tq + k][j]);
+                bvs[k] = lo2(sm.bc[4 * tq + k][q]);
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                h[0] = __builtin_fmaf(hw_exp2(dvs[k].x * a2[0]), h[0], dvs[k].y * bvs[k].x);
+                h[1] = __builtin_fmaf(hw_exp2(dvs[k].x * a2[1]), h[1], dvs[k].y * bvs[k].y);
+            }
         }
         wave_sync();
     };
@@ -291,16 +303,23 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
 #pragma unroll
         for (int tq = 0; tq < kT / 4; ++tq) {
             float acc[4];
-            f32x4 dvs[4], bvs[4];                       // the 4 steps' operands, read together
+            // the 4 steps' operands, read together; only the words used are read
+            float2 dvs[4];                              // (dlt, dlt*u)
+            f32x4 bvs[4];                               // (B0, B1, C0, C1); C only with a gate
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
-                dvs[k] = sm.dd[4 * tq + k][j];
-                bvs[k] = sm.bc[4 * tq + k][q];
+                dvs[k] = lo2(sm.dd[4 * tq + k][j]);
+                if (GATE) {
+                    bvs[k] = sm.bc[4 * tq + k][q];
+                } else {
+                    const float2 b2 = lo2(sm.bc[4 * tq + k][q]);
+                    bvs[k] = f32x4{b2.x, b2.y, 0.0f, 0.0f};
+                }
             }
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const int t = 4 * tq + k;
-                const f32x4 dv = dvs[k];
+                const float2 dv = dvs[k];
                 const f32x4 bv = bvs[k];
 #pragma unroll
                 for (int s = 0; s < 2; ++s) {
