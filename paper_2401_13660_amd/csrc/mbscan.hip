@@ -454,7 +454,19 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
         !mul_ok(rows, N, &state_elems))
         return MB_ERR_SHAPE;
     if (L >= (int64_t(1) << 31) || rows >= (int64_t(1) << 31)) return MB_ERR_SHAPE;
-    if (rows == 0) return MB_OK;
+    if (rows == 0) {
+        // no row: the parameter gradients are sums over nothing
+        if (D == 0) return MB_OK;
+        if (!dA || (Dskip && !dDskip) || (dt_bias && !ddt_bias)) return MB_ERR_NULL;
+        const void *f32z[] = {dA, dDskip, ddt_bias};
+        for (const void *q : f32z)
+            if (q && !aligned(q, 4)) return MB_ERR_ALIGN;
+        hipStream_t st0 = static_cast<hipStream_t>(stream);
+        hipError_t e0 = zero_async(dA, D * N, st0);
+        if (e0 == hipSuccess) e0 = zero_async(Dskip ? dDskip : nullptr, D, st0);
+        if (e0 == hipSuccess) e0 = zero_async(dt_bias ? ddt_bias : nullptr, D, st0);
+        return e0 == hipSuccess ? MB_OK : MB_ERR_HIP;
+    }
     if (!A || !dA || (Dskip && !dDskip) || (dt_bias && !ddt_bias)) return MB_ERR_NULL;
     if (L > 0 && (!u || !delta || !Bmat || !Cmat || !dy || !du || !ddelta || !dB || !dC || (z && !dz)))
         return MB_ERR_NULL;

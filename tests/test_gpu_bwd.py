@@ -65,7 +65,7 @@ def grads_case(inp, *, with_dhl=True, out_dtype=torch.float32, delta_softplus=Tr
 
 # (batch, dim, L): one chunk; several chunks with a ragged channel count (dead
 # lanes in the last 8-channel group); long enough that the reverse carry runs far.
-@pytest.mark.parametrize("shape", [(2, 196, 16), (3, 100, 48), (2, 196, 1008)])
+@pytest.mark.parametrize("shape", [(2, 196, 16), (3, 100, 48), (2, 196, 1008), (1, 5, 32), (1, 8, 16)])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_bwd_shapes(shape, dtype):
     inp = make_inputs(*shape, 16, dtype=dtype, seed=61, with_h0=True)
@@ -95,6 +95,30 @@ def test_bwd_random_A_and_bf16_gradients():
     inp = make_inputs(2, 96, 512, 16, dtype="bf16", seed=64, with_h0=True, A_kind="random")
     announce("bwd random A, bf16 dy and gradients")
     grads_case(inp, out_dtype=torch.bfloat16)
+
+
+def test_bwd_empty_sequence():
+    """L = 0: the state passes straight through (dh0 = dh_last) and every parameter
+    gradient is zero; a batch of 0 rows is a no-op."""
+    import paper_2401_13660_amd as mb
+    dev = "cuda:0"
+    nb, dim, N = 2, 24, 16
+    z3 = lambda *sh, dt=torch.bfloat16: torch.zeros(sh, dtype=dt, device=dev)
+    A = -torch.arange(1, N + 1, dtype=torch.float32, device=dev).repeat(dim, 1)
+    dhl = torch.randn((nb, dim, N), generator=torch.Generator().manual_seed(5)).to(dev)
+    announce("bwd L = 0")
+    g = mb.scan_bwd(z3(nb, dim, 0), z3(nb, dim, 0), A, z3(nb, N, 0), z3(nb, N, 0),
+                    z3(nb, dim, 0, dt=torch.float32), D=torch.ones(dim, device=dev),
+                    dt_bias=torch.zeros(dim, device=dev), dh_last=dhl)
+    torch.cuda.synchronize()
+    assert torch.equal(g["dh0"], dhl)
+    for k in ("dA", "dD", "ddt_bias"):
+        assert torch.count_nonzero(g[k]) == 0, k
+    g0 = mb.scan_bwd(z3(0, dim, 32), z3(0, dim, 32), A, z3(0, N, 32), z3(0, N, 32),
+                     z3(0, dim, 32, dt=torch.float32))
+    torch.cuda.synchronize()
+    assert g0["du"].numel() == 0
+    assert torch.count_nonzero(g0["dA"]) == 0, "dA over an empty batch must be zero"
 
 
 def test_bwd_deterministic():
