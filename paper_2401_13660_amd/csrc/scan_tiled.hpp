@@ -74,11 +74,15 @@ template <> struct Raw4<0> {
 constexpr int kDdRow = 9;       // 16-byte entries per row: 8 used + 1 pad
 constexpr int kBcRow = 10;      // 8 used + 2 pad
 constexpr int kPartRow = 9;     // 8 used + 1 pad
-struct WaveSmem {
-    f32x4 dd[kT / 2][kDdRow];                 // 2.25 KB
-    f32x4 bc[kT][kBcRow];                     // 5 KB
-    f32x4 part[kCh * (kT / 4)][kPartRow];     // 9 KB
+// SHORT: the tables of a sequence of one 16-timestep half chunk (the verify
+// shape), half the size, so that twice as many waves fit in a CU's LDS.
+template <bool SHORT> struct WaveSmemT {
+    static constexpr int kSteps = SHORT ? kT / 2 : kT;
+    f32x4 dd[kSteps / 2][kDdRow];             // 2.25 KB (SHORT: 1.1 KB)
+    f32x4 bc[kSteps][kBcRow];                 // 5 KB (2.5 KB)
+    f32x4 part[kCh * (kSteps / 4)][kPartRow]; // 9 KB (4.5 KB)
 };
+using WaveSmem = WaveSmemT<false>;
 
 // PREPASS = false: the scan itself.  With several time segments, the wave of
 //   segment s starts from h0 folded with the aggregates of segments 0..s-1.
@@ -90,11 +94,16 @@ struct WaveSmem {
 // POS = true (scan only): also record the states at p.pos (p.npos > 0).
 // CK = true (scan only): also store the state at every 16-timestep boundary in
 //   p.ck, the checkpoints the backward recomputes its chunks from.
-template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool PREPASS, bool POS, bool CK = false>
+// SHORT = true (scan only, seqlen 16): one half chunk per wave, with the
+//   half-size tables of WaveSmemT<true>.
+template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool PREPASS, bool POS, bool CK = false,
+          bool SHORT = false>
 __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len, float *carry) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    WaveSmem &sm = reinterpret_cast<WaveSmem *>(smem_raw)[wave];
+    using Smem = WaveSmemT<SHORT>;
+    Smem &sm = reinterpret_cast<Smem *>(smem_raw)[wave];
+    constexpr int kPS = Smem::kSteps / 4;              // part rows per channel
 
     const int lane = threadIdx.x & 63;
     const int j = lane >> 3;          // channel within the wave
@@ -198,7 +207,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
             if (PREPASS) dsum_chunk += dl;
             else acc4[k] = __builtin_fmaf(bcv[k][3], h[1], bcv[k][2] * h[0]);
         }
-        if (!PREPASS) sm.part[kT / 4 * j + TQ][q] = f32x4{acc4[0], acc4[1], acc4[2], acc4[3]};
+        if (!PREPASS) sm.part[kPS * j + TQ][q] = f32x4{acc4[0], acc4[1], acc4[2], acc4[3]};
     };
     auto load4 = [&](f32x4 (&ddv)[2], f32x4 (&bcv)[4], auto tq_c) {
         constexpr int TQ = decltype(tq_c)::value;
@@ -252,7 +261,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     };
 
     auto chunk = [&](Slot &sl, int64_t t0) {
-        const int nt = (int)(t_end - t0 < kT ? t_end - t0 : kT);   // valid timesteps, multiple of 16
+        const int nt = SHORT ? kT / 2 : (int)(t_end - t0 < kT ? t_end - t0 : kT);   // multiple of 16
 
         // ---- A: per-element work of timesteps 4q .. 4q+3 and B/C staging ------
         float xs[4], gs[4];
@@ -267,13 +276,17 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
                 xs[k] = x;
                 if (GATE && !PREPASS) gs[k] = silu_f32(sl.z.get(k));
             }
-            sm.dd[2 * q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
-            sm.dd[2 * q + 1][j] = f32x4{dl[2], dx[2], dl[3], dx[3]};
+            if (!SHORT || q < 4) {                  // SHORT: timesteps 16.. do not exist
+                sm.dd[2 * q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
+                sm.dd[2 * q + 1][j] = f32x4{dl[2], dx[2], dl[3], dx[3]};
+            }
         }
+        if (!SHORT || j < 4) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
-            sm.bc[st_t + k][q] = PREPASS ? f32x4{sl.B0.get(k), sl.B1.get(k), 0.0f, 0.0f}
-                                         : f32x4{sl.B0.get(k), sl.B1.get(k), sl.C0.get(k), sl.C1.get(k)};
+            for (int k = 0; k < 4; ++k)
+                sm.bc[st_t + k][q] = PREPASS ? f32x4{sl.B0.get(k), sl.B1.get(k), 0.0f, 0.0f}
+                                             : f32x4{sl.B0.get(k), sl.B1.get(k), sl.C0.get(k), sl.C1.get(k)};
+        }
         wave_sync();
 
         // refill this slot with the chunk after next while the recurrence runs
@@ -301,7 +314,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
             recur4(ddB, bcB, I1{});
             load4(ddB, bcB, I3{});
             recur4(ddA, bcA, I2{});
-            if (nt == kT) {
+            if (!SHORT && nt == kT) {
                 load4(ddA, bcA, I4{});
                 recur4(ddB, bcB, I3{});
                 if (CK) store_ck(t0 + 16);
@@ -326,9 +339,9 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
 
         // ---- C: sum the 8 partials of channel j at timesteps 4q .. 4q+3 --------
         if (4 * q < nt) {
-            f32x4 acc = sm.part[kT / 4 * j + q][0];
+            f32x4 acc = sm.part[kPS * j + q][0];
 #pragma unroll
-            for (int w = 1; w < kQ; ++w) acc += sm.part[kT / 4 * j + q][w];
+            for (int w = 1; w < kQ; ++w) acc += sm.part[kPS * j + q][w];
             float yv[4];
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -416,11 +429,17 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
     const int64_t waves = n_cg * p.batch * nseg;
     const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;
     void *args[] = {&p, &seg_len, &carry};
+    // One 16-timestep half chunk per wave (the verify shape): half-size tables.
+    const bool short_seq = p.seqlen == kT / 2 && nseg == 1 && !p.ck;
     const void *main_fn =
-        p.npos > 0 ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, true>)
-        : p.ck     ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false, true>)
-                   : reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false>);
-    e = hipLaunchKernel(main_fn, dim3((unsigned)blocks), dim3(kThreads), args, lds, st);
+        short_seq ? (p.npos > 0
+                         ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, true, false, true>)
+                         : reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false, false, true>))
+        : p.npos > 0 ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, true>)
+        : p.ck       ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false, true>)
+                     : reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false>);
+    const size_t main_lds = short_seq ? sizeof(WaveSmemT<true>) * kWavesPerGroup : lds;
+    e = hipLaunchKernel(main_fn, dim3((unsigned)blocks), dim3(kThreads), args, main_lds, st);
     if (carry) {
         const hipError_t f = hipFreeAsync(carry, st);
         if (e == hipSuccess) e = f;
