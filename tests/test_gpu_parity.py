@@ -46,6 +46,23 @@ def test_edge_lengths(L):
     run_case(inp)
 
 
+# L = 16: one half chunk per wave, the half-size-table instantiation (the
+# verify shape), across input and output types, with and without the gate and
+# softplus, and with dead lanes (dim 100).
+@pytest.mark.parametrize("dtype,gated,softplus,out", [("f32", True, True, torch.float32),
+                                                      ("bf16", False, True, torch.float32),
+                                                      ("bf16", True, True, torch.bfloat16),
+                                                      ("f32", False, False, torch.float32)])
+def test_one_half_chunk(dtype, gated, softplus, out):
+    inp = make_inputs(5, 100, 16, 16, dtype=dtype, seed=21, with_h0=True, gated=gated, with_bias=softplus)
+    if not softplus:                                  # dlt = delta as given: keep it small and positive
+        inp.delta = (np.abs(inp.delta) * np.float32(0.05)).astype(np.float32)
+    announce(f"L=16 (5, 100) {dtype} gated={gated} softplus={softplus} out={out}")
+    y, h = gpu_fwd(inp, out_dtype=out, delta_softplus=softplus)
+    check_against_oracle(inp, y, h, tol_y=BF16_OUT_TOL if out == torch.bfloat16 else 2e-3,
+                         delta_softplus=softplus)
+
+
 def test_dskip_zero_isolates_ssm_term():
     inp = make_inputs(2, 192, 2048, 16, dtype="bf16", seed=3, with_D=False)
     announce("Dskip = 0 (2, 192, 2048)")
