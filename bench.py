@@ -151,10 +151,25 @@ def bench_conv(args):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.graph:
+        # one step captured once (warm-up on a side stream first), then replayed:
+        # the per-call host work of the binding leaves the timed region
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        run = graph.replay
+    else:
+        run = step
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record()
     for _ in range(args.steps):
-        step()
+        run()
     stop.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
@@ -382,6 +397,8 @@ def main():
                          "mb_verify_rank (top-3 check of 16 drafted bytes over 256-way logits, batch 32); "
                          "bwd: one mb_scan_bwd (bf16 dy and activation gradients, fp32 parameter gradients); "
                          "train: one mb_scan_fwd_ckpt (bf16 y) and one mb_scan_bwd from its checkpoints")
+    ap.add_argument("--graph", action="store_true",
+                    help="fwd / step modes: capture one step in a HIP graph and time its replays")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the scan, run a plain device copy of MIB MiB (reference for HBM counters)")
     args = ap.parse_args()
@@ -448,10 +465,25 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.graph:
+        # one step captured once (warm-up on a side stream first), then replayed:
+        # the per-call host work of the binding leaves the timed region
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        run = graph.replay
+    else:
+        run = step
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record()
     for _ in range(args.steps):
-        step()
+        run()
     stop.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
@@ -471,7 +503,7 @@ def main():
         "config": {"workload": args.workload, "mode": args.mode,
                    **{k: v for k, v in WORKLOADS[args.workload].items()},
                    "gated": inp.z is not None, "h0": inp.h0 is not None, "h_last": want_h_last,
-                   "out_dtype": "f32", "parallelism": "single GPU"},
+                   "out_dtype": "f32", "parallelism": "single GPU", "hip_graph": bool(args.graph)},
         "elems_per_s": round(E / (ms * 1e-3), 1),
         "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
         "roofline": {"bound": "alu", "achieved": round(E / (ms * 1e-3) / 1e9, 2),
@@ -484,7 +516,8 @@ def main():
         # one-byte steps are bound by moving the state: report against HBM
         line["roofline"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                             "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                            "note": "includes host launch gaps between the per-byte calls"}
+                            "note": "one HIP graph of the per-byte calls" if args.graph
+                            else "includes host launch gaps between the per-byte calls"}
     if not args.no_cpu_baseline and args.mode == "fwd":
         cb = cpu_baseline(inp, y)
         line["cpu_baseline"] = {
