@@ -91,6 +91,36 @@ def measured_traffic(workload: str, sources=KERNEL_SOURCES):
     return rec.get("hbm_bytes_per_launch")
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def per_launch_ms(run, n, flush=None):
+    """Device time of each of n back-to-back launches, from events recorded between
+    consecutive launches on the launch stream (no synchronisation inside the loop,
+    so the host stays ahead and no idle time falls between the events).  With
+    ``flush``, that callable is enqueued before every launch, outside its events.
+    Returns the sorted times."""
+    import torch
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+    for i in range(n):
+        if flush is not None:
+            flush()
+        starts[i].record()
+        run()
+        ends[i].record()
+    torch.cuda.synchronize()
+    return sorted(a.elapsed_time(b) for a, b in zip(starts, ends))
+
+
 def cpu_baseline(inp, y_gpu):
     """fp64 oracle on this host's cores over the whole workload, batch by batch;
     also the parity gate for the GPU output of the same inputs."""
@@ -203,7 +233,7 @@ def bench_conv(args):
         ok = err <= 1e-5 + 2.0 ** -8 and np.array_equal(state_out.cpu().numpy().astype(np.float64), st_ref)
         line["cpu_baseline"] = {
             "value": round(nbytes / elapsed / 1e9, 3), "unit": "GB/s", "elems_per_s": round(E / elapsed, 1),
-            "cores": orc.max_threads(), "kind": "oracle",
+            "cores": orc.max_threads(), "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"whole workload: {c.batch} x {c.dim} rows of L={c.seqlen}, fp64, {elapsed:.1f} s"}
         line["parity"] = {"y_rel_err_vs_oracle": err, "ok": bool(ok)}
         if not ok:
@@ -314,7 +344,7 @@ def bench_bwd(args, train=False):
                   rel_err(grads["dB"][:nb].cpu().numpy(), ref["dB"]))
         ok = err <= 1e-4 + 2.0 ** -8
         line["cpu_baseline"] = {"value": round(Es / elapsed, 1), "unit": "elems/s", "cores": orc.max_threads(),
-                                "kind": "oracle",
+                                "kind": "oracle", "cpu_model": cpu_model(),
                                 "sample": f"batch element 0: {sub.dim} rows of L={sub.seqlen}, fp64, {elapsed:.1f} s"}
         line["parity"] = {"du_dB_rel_err_vs_oracle": err, "ok": bool(ok)}
         if not ok:
@@ -374,7 +404,7 @@ def bench_rank(args):
         elapsed = time.perf_counter() - t0
         ok = np.array_equal(ranks.cpu().numpy(), r_ref) and np.array_equal(acc.cpu().numpy(), a_ref)
         line["cpu_baseline"] = {"value": round(B * n / elapsed, 1), "unit": "bytes/s", "cores": 1,
-                                "kind": "oracle", "sample": f"the whole check, numpy, {elapsed * 1e3:.1f} ms"}
+                                "kind": "oracle", "cpu_model": cpu_model(), "sample": f"the whole check, numpy, {elapsed * 1e3:.1f} ms"}
         line["parity"] = {"ranks_and_accepted_equal": bool(ok), "ok": bool(ok)}
         if not ok:
             print(json.dumps(line))
@@ -487,6 +517,17 @@ def main():
     stop.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
+    # per-launch device times (median, min), and for a cache-resident workload the
+    # same after a 512 MB scrub write before every launch (inputs no longer in the
+    # 256 MB Infinity Cache)
+    pl = per_launch_ms(run, args.steps)
+    per_launch = {"median": round(pl[len(pl) // 2], 5), "min": round(pl[0], 5)}
+    if inp.batch * inp.dim * inp.seqlen * 10 < (256 << 20):
+        scrub = torch.empty(512 << 18, dtype=torch.float32, device=dev)
+        pf = per_launch_ms(run, args.steps, flush=lambda: scrub.fill_(1.0))
+        per_launch["flushed_median"] = round(pf[len(pf) // 2], 5)
+        per_launch["flushed_min"] = round(pf[0], 5)
+        del scrub
 
     E = inp.batch * inp.dim * inp.seqlen
     nbytes = algorithmic_bytes(inp, 4, want_h_last)
@@ -506,6 +547,7 @@ def main():
                    "out_dtype": "f32", "parallelism": "single GPU", "hip_graph": bool(args.graph)},
         "elems_per_s": round(E / (ms * 1e-3), 1),
         "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+        "ms_per_launch": per_launch,
         "roofline": {"bound": "alu", "achieved": round(E / (ms * 1e-3) / 1e9, 2),
                      "peak": round(ALU_PEAK_GELEMS, 1), "unit": "Gelem/s",
                      "frac": round(E / (ms * 1e-3) / 1e9 / ALU_PEAK_GELEMS, 4), "traffic": traffic,
@@ -522,7 +564,7 @@ def main():
         cb = cpu_baseline(inp, y)
         line["cpu_baseline"] = {
             "value": round(cb["elems_per_s"] * nbytes / E / 1e9, 3), "unit": "GB/s",
-            "elems_per_s": round(cb["elems_per_s"], 1), "cores": cb["threads"], "kind": "oracle",
+            "elems_per_s": round(cb["elems_per_s"], 1), "cores": cb["threads"], "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"whole workload: {inp.batch} x {inp.dim} rows of L={inp.seqlen}, fp64, "
                       f"{cb['elapsed']:.1f} s",
         }
