@@ -121,6 +121,25 @@ def per_launch_ms(run, n, flush=None):
     return sorted(a.elapsed_time(b) for a, b in zip(starts, ends))
 
 
+def copy_bandwidth_gbs(dev, mib=1024, reps=5) -> float:
+    """Bandwidth of a plain device copy (mib MiB read + mib MiB written): the
+    practical ceiling that a streaming kernel is also compared with."""
+    import torch
+    src = torch.ones((mib << 20) // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    secs = a.elapsed_time(b) / reps * 1e-3
+    del src, dst
+    return 2 * (mib << 20) / secs / 1e9
+
+
 def cpu_baseline(inp, y_gpu):
     """fp64 oracle on this host's cores over the whole workload, batch by batch;
     also the parity gate for the GPU output of the same inputs."""
@@ -529,6 +548,7 @@ def main():
         per_launch["flushed_min"] = round(pf[0], 5)
         del scrub
 
+    copy_gbs = copy_bandwidth_gbs(dev)
     E = inp.batch * inp.dim * inp.seqlen
     nbytes = algorithmic_bytes(inp, 4, want_h_last)
     if args.mode == "step":
@@ -548,6 +568,7 @@ def main():
         "elems_per_s": round(E / (ms * 1e-3), 1),
         "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
         "ms_per_launch": per_launch,
+        "copy_gbs": round(copy_gbs, 1), "frac_of_copy": round(gbs / copy_gbs, 4),
         "roofline": {"bound": "alu", "achieved": round(E / (ms * 1e-3) / 1e9, 2),
                      "peak": round(ALU_PEAK_GELEMS, 1), "unit": "Gelem/s",
                      "frac": round(E / (ms * 1e-3) / 1e9 / ALU_PEAK_GELEMS, 4), "traffic": traffic,
