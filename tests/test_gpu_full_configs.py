@@ -14,11 +14,16 @@ from paper_2401_13660_amd.inputs import workload
 pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not has_gpu(), reason="needs a GPU")]
 
 
+# With Dskip = 0 the output is the SSM term alone: |D u| (about 1) no longer
+# dominates |C h| (about 0.3), so the same bar on y checks the scan more tightly.
+@pytest.mark.parametrize("dskip", [True, False], ids=["dskip", "dskip0"])
 @pytest.mark.parametrize("name", ["mambabyte353m_L8192", "mambabyte972m_L8192", "mambabyte1p6b_L65536"])
-def test_full_size_every_row(name):
+def test_full_size_every_row(name, dskip):
     inp = workload(name)
+    if not dskip:
+        inp.Dskip = None
     nb, dim, L = inp.u.shape
-    announce(f"{name} full size {inp.u.shape}, every row")
+    announce(f"{name} full size {inp.u.shape}, every row, Dskip {'on' if dskip else '0'}")
     y, h = gpu_fwd(inp)
     rows_total = nb * dim
     yg = y.float().cpu().numpy().reshape(rows_total, L)
@@ -34,4 +39,4 @@ def test_full_size_every_row(name):
         worst_y, worst_h = max(worst_y, ey), max(worst_h, eh)
         assert ey <= 2e-3, f"rows {r0}..: y relative error {ey:.3e}"
         assert eh <= 1e-4, f"rows {r0}..: h_last relative error {eh:.3e}"
-    print(f"[{name}] every row: y {worst_y:.2e}, h_last {worst_h:.2e}", flush=True)
+    print(f"[{name} dskip={dskip}] every row: y {worst_y:.2e}, h_last {worst_h:.2e}", flush=True)
