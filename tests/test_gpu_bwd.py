@@ -63,9 +63,11 @@ def grads_case(inp, *, with_dhl=True, out_dtype=torch.float32, delta_softplus=Tr
     return errs
 
 
-# (batch, dim, L): one chunk; several chunks with a ragged channel count (dead
-# lanes in the last 8-channel group); long enough that the reverse carry runs far.
-@pytest.mark.parametrize("shape", [(2, 196, 16), (3, 100, 48), (2, 196, 1008), (1, 5, 32), (1, 8, 16)])
+# (batch, dim, L): one chunk; several chunks with dead lanes in the last
+# 8-channel group; a long reverse carry; a single ragged group; one group; more
+# than 1,024 channel groups (more waves than SIMDs), with and without dead lanes.
+@pytest.mark.parametrize("shape", [(2, 196, 16), (3, 101, 48), (2, 197, 1008), (1, 5, 32), (1, 8, 16),
+                                   (9, 1001, 32), (9, 1024, 16)])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_bwd_shapes(shape, dtype):
     inp = make_inputs(*shape, 16, dtype=dtype, seed=61, with_h0=True)
@@ -121,9 +123,10 @@ def test_bwd_empty_sequence():
     assert torch.count_nonzero(g0["dA"]) == 0, "dA over an empty batch must be zero"
 
 
-def test_bwd_deterministic():
+@pytest.mark.parametrize("shape", [(2, 128, 512), (9, 1001, 64)], ids=["small", "many_groups"])
+def test_bwd_deterministic(shape):
     import paper_2401_13660_amd as mb
-    inp = make_inputs(2, 128, 512, 16, dtype="bf16", seed=65, with_h0=True)
+    inp = make_inputs(*shape, 16, dtype="bf16", seed=65, with_h0=True)
     t = {k: dev_tensor(v) for k, v in inp.arrays().items()}
     dy = torch.randn(inp.u.shape, generator=torch.Generator().manual_seed(0)).to("cuda:0")
     announce("bwd determinism")
@@ -135,10 +138,11 @@ def test_bwd_deterministic():
             assert torch.equal(outs[0][k], outs[1][k]), f"{k} differs between runs"
 
 
-def test_bwd_972m_layer_every_row():
-    """The MambaByte-972M layer shape at full size: every gradient of every row."""
-    inp = workload("mambabyte972m_L8192", seed=0)
-    announce("bwd 972M layer (4, 3584, 8192), every row")
+@pytest.mark.parametrize("name", ["mambabyte353m_L8192", "mambabyte972m_L8192"])
+def test_bwd_layer_every_row(name):
+    """The 353M and 972M layer shapes at full size: every gradient of every row."""
+    inp = workload(name, seed=0)
+    announce(f"bwd {name} {inp.u.shape}, every row")
     grads_case(inp, with_dhl=False)
 
 
@@ -174,7 +178,7 @@ def test_fwd_checkpoints_match_oracle_states(shape, dtype):
     assert e <= 1e-4, f"checkpoints: relative error {e:.3e}"
 
 
-@pytest.mark.parametrize("shape,gated", [((2, 196, 512), True), ((1, 64, 1024), False)])
+@pytest.mark.parametrize("shape,gated", [((2, 196, 512), True), ((1, 64, 1024), False), ((9, 1001, 64), True)])
 def test_bwd_from_forward_checkpoints(shape, gated):
     """The backward from the forward's checkpoints: oracle parity, and the same
     gradients as the backward that recomputes its checkpoints."""
