@@ -299,3 +299,27 @@ def test_binding_fails_loudly_without_library(tmp_path):
             B.load_library(str(tmp_path / "missing.so"))
     finally:
         B._lib = saved
+
+
+def test_header_is_c_and_matches_the_binding(tmp_path):
+    """include/mbscan.h compiles as C99 (-pedantic), and its structs have the
+    layout the ctypes binding declares."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    src = tmp_path / "layout.c"
+    src.write_text(
+        '#include "mbscan.h"\n#include <stddef.h>\n#include <stdio.h>\n'
+        "int main(void) {\n"
+        '  printf("%zu %zu %zu %zu %zu %zu\\n", sizeof(mb_scan_desc), offsetof(mb_scan_desc, in_dtype),\n'
+        "         offsetof(mb_scan_desc, reserved), sizeof(mb_conv_desc), offsetof(mb_conv_desc, width),\n"
+        "         offsetof(mb_conv_desc, reserved2));\n"
+        "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-pedantic", "-I", os.path.dirname(HEADER), str(src),
+                    "-o", str(exe)], check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()]
+    want = [ctypes.sizeof(B.ScanDesc), B.ScanDesc.in_dtype.offset, B.ScanDesc.reserved.offset,
+            ctypes.sizeof(B.ConvDesc), B.ConvDesc.width.offset, B.ConvDesc.reserved2.offset]
+    assert got == want, f"C layout {got} != ctypes layout {want}"
