@@ -383,6 +383,34 @@ def pin_bwd_finite_differences(orc):
                     f"{gname}{idx} seed {seed}: analytic {an:.9g} vs finite difference {fd:.9g}"
 
 
+def pin_bwd_geometric(orc):
+    """Constant dlt, B, C, x, no gate, h0 = 0, dy = 1: every gradient in closed form.
+
+    With a = e^(dlt A) and b = dlt B x the forward is the geometric series
+    h_t = b (1 - a^(t+1)) / (1 - a), and the gradient of the loss with respect to
+    h_t is lambda_t = C (1 - a^(L-t)) / (1 - a) (each later output sees h_t
+    decayed by a per step).  The derivatives of eq. (2) with the Euler input term
+    then read off as sums of products of these closed forms."""
+    L, d, x, Ds = 20, 0.3, 0.7, 0.9
+    A = np.array([-1.0, -0.5])
+    Bn, Cn = np.array([0.5, -1.2]), np.array([1.3, 0.4])
+    a, b = np.exp(d * A), d * Bn * x
+    t = np.arange(L)[:, None]
+    h = b * (1 - a ** (t + 1)) / (1 - a)                    # (L, N): h_t
+    h_prev = b * (1 - a ** t) / (1 - a)                     # h_{t-1}, zero at t = 0
+    lam = Cn * (1 - a ** (L - t)) / (1 - a)                 # (L, N): lambda_t
+    want = dict(
+        du=Ds + d * (lam * Bn).sum(axis=1),
+        ddelta=(lam * (A * a * h_prev + x * Bn)).sum(axis=1),
+        dA=(d * lam * a * h_prev).sum(axis=0),
+        dB=(lam * d * x).T, dC=h.T, dD=np.array([L * x]), dh0=a * lam[0])
+    g = orc.scan_bwd(np.full((1, 1, L), x), np.full((1, 1, L), d), A[None, :],
+                     np.repeat(Bn[None, :, None], L, axis=2), np.repeat(Cn[None, :, None], L, axis=2),
+                     np.ones((1, 1, L)), Dskip=np.array([Ds]), h0=np.zeros((1, 1, 2)), delta_softplus=False)
+    for k, w in want.items():
+        _close(np.asarray(g[k]).ravel(), np.asarray(w).ravel(), 1e-12, f"bwd geometric {k}")
+
+
 def pin_bwd_linearity(orc):
     """Gradients are linear in the incoming (dy, dh_last)."""
     c = _rand_case(54, nb=2, dim=2, L=9, N=3)
@@ -472,5 +500,5 @@ ALL_PINS = [
     pin_tuple_scan, pin_separability, pin_linearity, pin_step_equals_fwd, pin_limits,
     pin_softplus_extremes, pin_states_at_positions,
     pin_conv_library, pin_conv_impulse, pin_conv_split_and_step,
-    pin_bwd_finite_differences, pin_bwd_linearity,
+    pin_bwd_finite_differences, pin_bwd_geometric, pin_bwd_linearity,
 ]
