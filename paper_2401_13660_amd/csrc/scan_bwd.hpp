@@ -95,7 +95,6 @@ struct WaveSmem {
     f32x4 bc[kT][kQ + 2];             // (B[2q], B[2q+1], C[2q], C[2q+1]) of timestep t
     f32x4 pa[kCh * (kT / 4)][kQ + 1]; // per-state-pair partials, 4 timesteps per entry
     f32x4 pb[kCh * (kT / 4)][kQ + 1];
-    f32x4 x[4][kQ][kCh + 1];          // dB / dC contributions of 4 timesteps, summed over j
 };
 
 // The first two words of a 16-byte LDS entry, as one 8-byte read.  (Reading the
@@ -135,6 +134,20 @@ __device__ __forceinline__ float half_swap_sum(float a, float b) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
     const unsigned r0 = r[0], r1 = r[1];
     return __uint_as_float(r0) + __uint_as_float(r1);
+}
+
+// The same over lanes l and l ^ 16 (v_permlane16_swap exchanges the odd 16-lane
+// rows of its first operand with the even rows of its second): even rows receive
+// a's sum, odd rows b's.
+__device__ __forceinline__ float row_swap_sum(float a, float b) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+    const unsigned r0 = r[0], r1 = r[1];
+    return __uint_as_float(r0) + __uint_as_float(r1);
+}
+
+// v + the value of lane l ^ 8 (a DPP rotation by 8 inside each 16-lane row).
+__device__ __forceinline__ float add_xor8(float v) {
+    return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false));
 }
 
 // The wave's (batch, channel group) from a workgroup renumbered so that each of
@@ -347,9 +360,17 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
         wave_sync();                                    // pa is rewritten below
 
         // ---- R: the adjoint recurrence, timesteps 15 .. 0 -------------------------
+        // The dB / dC terms of each step are summed over the wave's 8 channels in
+        // registers: the channel bits 5, 4 and 3 of the lane meet in a 32-lane swap,
+        // a 16-lane swap and a rotation by 8, after which lane (b5, b4, b3, q) holds
+        // entry 2 b5 + b4 of state pair q's (dB[2q], dC[2q], dB[2q+1], dC[2q+1]),
+        // the same for b3 = 0 and 1; lanes with b3 = 0 store the even step of a pair,
+        // lanes with b3 = 1 the odd one.
+        const int b3 = (lane >> 3) & 1;
+        float *const pl = pbc + t0 * (kQ * 4) + b3 * (kQ * 4) + q * 4 + (((lane >> 5) << 1) | ((lane >> 4) & 1));
 #pragma unroll
         for (int tq = kT / 4 - 1; tq >= 0; --tq) {
-            float pu[4], pd[4];
+            float pu[4], pd[4], tot_hi = 0.0f;
             f32x4 dvs[4], bvs[4];                       // the 4 steps' operands, read together
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -363,7 +384,14 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
                 const f32x4 bv = bvs[k];               // (B0, B1, C0, C1)
                 const float lam0 = __builtin_fmaf(dv.z, bv.z, carry[0]);
                 const float lam1 = __builtin_fmaf(dv.z, bv.w, carry[1]);
-                sm.x[k][q][j] = f32x4{lam0 * dv.y, lam1 * dv.y, dv.z * hb[t + 1][0], dv.z * hb[t + 1][1]};
+                const float sb = half_swap_sum(lam0 * dv.y, lam1 * dv.y);                  // dB: b5 picks the state
+                const float sc = half_swap_sum(dv.z * hb[t + 1][0], dv.z * hb[t + 1][1]);  // dC
+                const float tot = add_xor8(row_swap_sum(sb, sc));                          // b4 picks dB or dC
+                if (k & 1) {
+                    tot_hi = tot;
+                } else {                                // steps k, k + 1: b3 = 0 stores k, b3 = 1 stores k + 1
+                    pl[(4 * tq + k) * (kQ * 4)] = b3 ? tot_hi : tot;
+                }
                 const float u0 = __builtin_fmaf(lam1, bv.y, lam0 * bv.x);
                 const float w0 = lam0 * ab[t][0] * hb[t][0];
                 const float w1 = lam1 * ab[t][1] * hb[t][1];
@@ -376,23 +404,8 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
             }
             sm.pa[4 * j + tq][q] = f32x4{pu[0], pu[1], pu[2], pu[3]};
             sm.pb[4 * j + tq][q] = f32x4{pd[0], pd[1], pd[2], pd[3]};
-            wave_sync();
-            // dB / dC of timesteps 4tq .. 4tq+3 summed over the wave's 8 channels:
-            // lane (half, k, q') sums channels 4 half .. 4 half + 3; the halves meet
-            // in a swap that leaves state 2q' (dB, dC) in half 0 and state 2q'+1 in
-            // half 1, and every lane writes its 8 bytes of the partial.
-            {
-                const int half = lane >> 5, kk = (lane >> 3) & 3, qq = lane & 7;
-                f32x4 sum = sm.x[kk][qq][4 * half];
-#pragma unroll
-                for (int i = 1; i < 4; ++i) sum += sm.x[kk][qq][4 * half + i];
-                const float db = half_swap_sum(sum.x, sum.y);   // dB[2q'] | dB[2q'+1]
-                const float dc = half_swap_sum(sum.z, sum.w);   // dC[2q'] | dC[2q'+1]
-                *reinterpret_cast<float2 *>(pbc + ((t0 + 4 * tq + kk) * kQ + qq) * 4 + 2 * half) =
-                    make_float2(db, dc);
-            }
-            wave_sync();                                // x is rewritten by the next step
         }
+        wave_sync();                                    // pa / pb are read below
 
         // ---- C2: du and ddelta of timesteps 2q, 2q+1 ------------------------------
         {
