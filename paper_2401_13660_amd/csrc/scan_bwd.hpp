@@ -21,8 +21,8 @@
 //               reverse; per chunk: the per-element terms (A), the chunk's forward
 //               from its checkpoint keeping h_t and abar_t in VGPRs (F), s_t and
 //               dz (C1), the adjoint recurrence backwards (R), then du and ddelta
-//               (C2).  dB and dC are summed over the wave's 8 channels through
-//               LDS every 4 timesteps and written as one partial per wave;
+//               (C2).  dB and dC are summed over the wave's 8 channels in
+//               registers (lane swaps) and written as one partial per wave;
 //   bwd_finish  sums the dB / dC partials over channel groups and dA, dDskip,
 //               dbias over the batch (no atomics: results are deterministic).
 #pragma once
@@ -89,7 +89,8 @@ template <int DT> __device__ __forceinline__ void store2(void *base, int64_t off
     }
 }
 
-// Private LDS area of one wave; padded rows keep reads and writes conflict-free.
+// Private LDS area of one wave (13.75 KB); padded rows spread reads and writes
+// over the banks.
 struct WaveSmem {
     f32x4 dd[kT][kCh + 1];            // (dlt, dlt*u, ds, u) of timestep t, channel j
     f32x4 bc[kT][kQ + 2];             // (B[2q], B[2q+1], C[2q], C[2q+1]) of timestep t
