@@ -6,12 +6,17 @@ binding over it.  ``scan_fwd``, ``scan_step``, the backward ``scan_bwd``, the ca
 convolution upstream
 of the scan, ``conv1d`` and ``conv1d_step``, and the top-beta check that ends a
 speculative verification, ``verify_rank``, are loaded on first use.
+``selective_scan`` is the scan as a differentiable torch operation (forward with
+checkpoints, backward from them).
 """
 __all__ = ["scan_fwd", "scan_step", "scan_bwd", "conv1d", "conv1d_step", "verify_rank", "load_library",
-           "MBScanError"]
+           "MBScanError", "selective_scan"]
 
 
 def __getattr__(name):
+    if name == "selective_scan":
+        from .autograd import selective_scan
+        return selective_scan
     if name in __all__:
         from . import _binding
         return getattr(_binding, name)
