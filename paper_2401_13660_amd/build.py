@@ -20,6 +20,9 @@ FLAGS = [
     # Packed-fp32 instructions stay off: every fp32 operation is a plain VALU op.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
+    # A name that shadows another (a lambda local over a captured variable among
+    # them) is an error: one such shadow once sent LDS writes to a private array.
+    "-Werror=shadow-all",
 ]
 
 

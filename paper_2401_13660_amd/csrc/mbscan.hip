@@ -160,6 +160,23 @@ hipError_t zero_async(float *p, int64_t n, hipStream_t st) {
                            dim3(256), args, 0, st);
 }
 
+// The backward's dB/dC partials come one per 8-channel group, or one per
+// workgroup of 4 groups: when the group count is a multiple of 4 (no workgroup
+// spans two batch elements) and there are at least 1,536 waves (1.5 per SIMD, so
+// that the other workgroup's waves fill a SIMD while one waits at the
+// workgroup's barrier every 4 steps), the workgroup sums its waves' terms in LDS.
+bool bwd_workgroup_sum(int64_t batch, int64_t dim) {
+    namespace W = mbs::bwd;
+    const int64_t n_cg = (dim + W::kCh - 1) / W::kCh;
+    return n_cg % W::kWaves == 0 && n_cg * batch >= 1536;
+}
+
+int64_t bwd_partial_groups(int64_t batch, int64_t dim) {
+    namespace W = mbs::bwd;
+    const int64_t n_cg = (dim + W::kCh - 1) / W::kCh;
+    return bwd_workgroup_sum(batch, dim) ? n_cg / W::kWaves : n_cg;
+}
+
 template <int IN, int OUT, bool GATE, bool SP>
 hipError_t bwd_launch(mbs::bwd::BwdParams &p, bool have_ck, float *dA, float *dB, float *dC, float *dD,
                       float *dbias, hipStream_t st) {
@@ -173,10 +190,14 @@ hipError_t bwd_launch(mbs::bwd::BwdParams &p, bool have_ck, float *dA, float *dB
     if (!have_ck)
         e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_ckpt<IN, SP>), grid, block, args, lds, st);
     if (e != hipSuccess) return e;
-    e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_bwd<IN, OUT, GATE, SP>), grid, block, args, lds,
-                        st);
+    if (bwd_workgroup_sum(p.batch, p.dim))
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_bwd<IN, OUT, GATE, SP, true>), grid, block,
+                            args, lds, st);                      // + its static exchange area
+    else
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_bwd<IN, OUT, GATE, SP, false>), grid, block,
+                            args, lds, st);
     if (e != hipSuccess) return e;
-    int64_t ncg = n_cg;
+    int64_t ncg = bwd_partial_groups(p.batch, p.dim);
     void *fargs[] = {&p, &dB, &dC, &ncg};
     const int64_t nbc = p.batch * p.seqlen * W::kQ;
     e = hipLaunchKernel(reinterpret_cast<const void *>(&W::bwd_finish_bc), dim3((unsigned)((nbc + 255) / 256)),
@@ -514,7 +535,7 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     }
 
     namespace W = mbs::bwd;
-    const int64_t n_cg = (D + W::kCh - 1) / W::kCh;
+    const int64_t n_cg = bwd_partial_groups(B, D);       // dB/dC partials per (batch, t)
     const size_t ck_b = ck ? 0 : (size_t)(L / W::kT) * (size_t)rows * W::kN * 4;
     const size_t bcp_b = (size_t)n_cg * (size_t)B * (size_t)L * W::kQ * 4 * 4;
     const size_t row_b = (size_t)rows * (W::kN + 2) * 4;

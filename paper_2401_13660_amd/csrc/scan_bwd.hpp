@@ -236,10 +236,20 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
 }
 
 // ---- the backward pass -----------------------------------------------------------
-template <int IN, int OUT, bool GATE, bool SOFTPLUS>
-__global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
+// Floats of the workgroup's dB/dC exchange area (WG = true): two buffers of
+// 4 waves x 2 step pairs x 64 lanes.
+constexpr int kWgXchg = 2 * kWaves * 2 * 64;
+
+// WG = true (the number of 8-channel groups is a multiple of 4, so the 4 waves of
+// a workgroup are 4 consecutive groups of one batch element): the waves also
+// sum their dB/dC terms with each other through LDS every 4 steps, one barrier
+// per 4 steps, and the workgroup writes one partial per 32 channels.
+template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool WG = false>
+__global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 waves per SIMD: <= 256 VGPRs
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    WaveSmem &sm = reinterpret_cast<WaveSmem *>(smem_raw)[__builtin_amdgcn_readfirstlane(threadIdx.x >> 6)];
+    __shared__ float wg_sums[WG ? kWgXchg : 1];         // WG: the workgroup's dB/dC exchange area
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    WaveSmem &sm = reinterpret_cast<WaveSmem *>(smem_raw)[wave];
     const int lane = threadIdx.x & 63, j = lane >> 3, q = lane & 7, n0 = 2 * q;
     const int64_t n_cg = (p.dim + kCh - 1) / kCh;
     const int64_t wid = wave_id();
@@ -260,7 +270,8 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
     }
     float sum_dD = 0.0f, sum_dbias = 0.0f;
     const int64_t act = row * L, bcr = (b * kN + n0) * L;
-    float *pbc = p.part_bc + ((cg * p.batch + b) * L) * (kQ * 4);
+    float *pbc = p.part_bc + (((WG ? cg / kWaves : cg) * p.batch + b) * L) * (kQ * 4);
+    int buf = 0;                                        // WG: the exchange buffer in use
 
     // Loads run two chunks ahead (in processing order: backwards in time) in two
     // static register slots, clamped at the sequence start, never branched.
@@ -391,7 +402,9 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
                 if (k & 1) {
                     tot_hi = tot;
                 } else {                                // steps k, k + 1: b3 = 0 stores k, b3 = 1 stores k + 1
-                    pl[(4 * tq + k) * (kQ * 4)] = b3 ? tot_hi : tot;
+                    const float v = b3 ? tot_hi : tot;
+                    if (WG) wg_sums[((buf * kWaves + wave) * 2 + (k >> 1)) * 64 + lane] = v;
+                    else pl[(4 * tq + k) * (kQ * 4)] = v;
                 }
                 const float u0 = __builtin_fmaf(lam1, bv.y, lam0 * bv.x);
                 const float w0 = lam0 * ab[t][0] * hb[t][0];
@@ -405,6 +418,22 @@ __global__ __launch_bounds__(kThreads) void scan_bwd(BwdParams p) {
             }
             sm.pa[4 * j + tq][q] = f32x4{pu[0], pu[1], pu[2], pu[3]};
             sm.pb[4 * j + tq][q] = f32x4{pd[0], pd[1], pd[2], pd[3]};
+            if (WG) {
+                // Every wave's 128 sums of this group are in wg_sums[buf]; wave w adds up
+                // the 4 waves' values of source lanes 32 (w & 1) .. + 31 of step pair
+                // w >> 1 (fixed order: deterministic) and writes them.  The buffers
+                // alternate, so the next group's writes never meet these reads: a wave
+                // passes the next barrier only after all have finished reading here.
+                __syncthreads();
+                if (lane < 32) {
+                    const int i = wave >> 1, l = (wave & 1) * 32 + lane;
+                    const float *x0 = wg_sums + (buf * kWaves * 2 + i) * 64 + l;
+                    const float sum = (x0[0] + x0[2 * 64]) + (x0[4 * 64] + x0[6 * 64]);
+                    const int lslot = ((l >> 5) << 1) | ((l >> 4) & 1);
+                    pbc[(t0 + 4 * tq + 2 * i + ((l >> 3) & 1)) * (kQ * 4) + (l & 7) * 4 + lslot] = sum;
+                }
+                buf ^= 1;
+            }
         }
         wave_sync();                                    // pa / pb are read below
 

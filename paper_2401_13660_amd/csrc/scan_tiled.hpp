@@ -114,8 +114,8 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     // renumber them so that an XCD works on a contiguous range of (batch,
     // channel) groups and the B/C rows of a batch stay in one or two L2s.
     const int64_t per_xcd = (int64_t)gridDim.x / 8;
-    const int64_t k = blockIdx.x;
-    const int64_t lwg = k < per_xcd * 8 ? (k % 8) * per_xcd + k / 8 : k;
+    const int64_t blk = blockIdx.x;
+    const int64_t lwg = blk < per_xcd * 8 ? (blk % 8) * per_xcd + blk / 8 : blk;
     const int64_t wid = lwg * kWavesPerGroup + wave;
     if (wid >= n_cg * p.batch * (PREPASS ? nseg - 1 : nseg)) return;   // whole wave leaves together
     const int64_t cg = wid % n_cg;

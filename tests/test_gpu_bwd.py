@@ -65,9 +65,11 @@ def grads_case(inp, *, with_dhl=True, out_dtype=torch.float32, delta_softplus=Tr
 
 # (batch, dim, L): one chunk; several chunks with dead lanes in the last
 # 8-channel group; a long reverse carry; a single ragged group; one group; more
-# than 1,024 channel groups (more waves than SIMDs), with and without dead lanes.
+# than 1,024 channel groups (more waves than SIMDs), with and without dead lanes;
+# at least 1,536 groups, a multiple of 4 per batch element, where the 4 waves of a
+# workgroup also sum their dB/dC terms with each other, with and without dead lanes.
 @pytest.mark.parametrize("shape", [(2, 196, 16), (3, 101, 48), (2, 197, 1008), (1, 5, 32), (1, 8, 16),
-                                   (9, 1001, 32), (9, 1024, 16)])
+                                   (9, 1001, 32), (9, 1024, 16), (12, 1024, 16), (12, 1020, 32)])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_bwd_shapes(shape, dtype):
     inp = make_inputs(*shape, 16, dtype=dtype, seed=61, with_h0=True)
@@ -123,7 +125,8 @@ def test_bwd_empty_sequence():
     assert torch.count_nonzero(g0["dA"]) == 0, "dA over an empty batch must be zero"
 
 
-@pytest.mark.parametrize("shape", [(2, 128, 512), (9, 1001, 64)], ids=["small", "many_groups"])
+@pytest.mark.parametrize("shape", [(2, 128, 512), (9, 1001, 64), (12, 1020, 64)],
+                         ids=["small", "many_groups", "workgroup_sum"])
 def test_bwd_deterministic(shape):
     import paper_2401_13660_amd as mb
     inp = make_inputs(*shape, 16, dtype="bf16", seed=65, with_h0=True)
@@ -178,7 +181,8 @@ def test_fwd_checkpoints_match_oracle_states(shape, dtype):
     assert e <= 1e-4, f"checkpoints: relative error {e:.3e}"
 
 
-@pytest.mark.parametrize("shape,gated", [((2, 196, 512), True), ((1, 64, 1024), False), ((9, 1001, 64), True)])
+@pytest.mark.parametrize("shape,gated", [((2, 196, 512), True), ((1, 64, 1024), False), ((9, 1001, 64), True),
+                                         ((12, 1024, 32), True)])
 def test_bwd_from_forward_checkpoints(shape, gated):
     """The backward from the forward's checkpoints: oracle parity, and the same
     gradients as the backward that recomputes its checkpoints."""
