@@ -98,6 +98,16 @@ struct WaveSmem {
     f32x4 pb[kCh * (kT / 4)][kQ + 1];
 };
 
+// softplus(v) (as softplus_f32) and its derivative sigmoid(v) from the one
+// exponential e = e^-|v|: sigmoid(v) = 1 / (1 + e) for v >= 0, e / (1 + e) below.
+__device__ __forceinline__ void softplus_and_sigmoid(float v, float &sp, float &sg) {
+    const float e = hw_exp2(-__builtin_fabsf(v) * kLog2e);
+    const float w = 1.0f + e;
+    const float c = e - (w - 1.0f);
+    sp = __builtin_fmaxf(v, 0.0f) + __builtin_fmaf(hw_log2(w), kLn2, c);
+    sg = (v >= 0.0f ? 1.0f : e) * hw_rcp(w);
+}
+
 // The first two words of a 16-byte LDS entry, as one 8-byte read.  (Reading the
 // whole entry when two words are used lets the compiler reuse the unused half of
 // the destination for the next read, which then has to wait for this one.)
@@ -303,16 +313,22 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
         float hb[kT + 1][2], ab[kT][2];                 // h_{t-1} .. h_{t+15}; abar_t
         hb[0][0] = live ? sl.ck0 : 0.0f;
         hb[0][1] = live ? sl.ck1 : 0.0f;
-        float xs[2], dyv[2], zv[2], sg[2], dlv[2], dsv[2];
+        float xs[2], dyv[2], dsilu[2], sg[2], dlv[2], dsv[2];
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
             const float x = sl.u.get(k);
             const float v = sl.dl.get(k) + bias;
-            const float dl = SOFTPLUS ? softplus_f32(v) : v;
-            sg[k] = SOFTPLUS ? hw_rcp(1.0f + hw_exp2(-v * kLog2e)) : 1.0f;   // softplus'(v)
+            float dl = v;
+            sg[k] = 1.0f;
+            if (SOFTPLUS) softplus_and_sigmoid(v, dl, sg[k]);          // softplus'(v) = sigmoid(v)
             dyv[k] = sl.dy.get(k);
-            zv[k] = GATE ? sl.z.get(k) : 0.0f;
-            const float g = GATE ? silu_f32(zv[k]) : 1.0f;
+            float g = 1.0f;
+            if (GATE) {                                 // silu(z) and silu'(z) from one sigmoid
+                const float z = sl.z.get(k);
+                const float sz = hw_rcp(1.0f + hw_exp2(-z * kLog2e));
+                g = z * sz;
+                dsilu[k] = sz * __builtin_fmaf(z, 1.0f - sz, 1.0f);
+            }
             const float ds = dyv[k] * g;
             xs[k] = x;
             dlv[k] = dl;
@@ -364,8 +380,7 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
 #pragma unroll
             for (int k = 0; k < 2; ++k) {
                 const float s = __builtin_fmaf(dskip, xs[k], sp[k]);
-                const float sgz = hw_rcp(1.0f + hw_exp2(-zv[k] * kLog2e));
-                dzv[k] = dyv[k] * s * sgz * __builtin_fmaf(zv[k], 1.0f - sgz, 1.0f);
+                dzv[k] = dyv[k] * s * dsilu[k];
             }
             if (live) store2<OUT>(p.dz, act + t0 + 2 * q, dzv[0], dzv[1]);
         }
