@@ -83,6 +83,14 @@ template <bool SHORT> struct WaveSmemT {
     f32x4 part[kCh * (kSteps / 4)][kPartRow]; // 9 KB (4.5 KB)
 };
 using WaveSmem = WaveSmemT<false>;
+// The pre-pass needs neither C nor the output partials.  It stages B two
+// timesteps per entry, and the smaller area lets more waves share a CU:
+//   b2    row r = timesteps 2r, 2r+1; entry q = (B[2q], B[2q+1]) at 2r, then at 2r+1
+struct WaveSmemPre {
+    static constexpr int kSteps = kT;
+    f32x4 dd[kT / 2][kDdRow];                 // 2.25 KB
+    f32x4 b2[kT / 2][kDdRow];                 // 2.25 KB
+};
 
 // PREPASS = false: the scan itself.  With several time segments, the wave of
 //   segment s starts from h0 folded with the aggregates of segments 0..s-1.
@@ -101,7 +109,7 @@ template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool PREPASS, bool POS, boo
 __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len, float *carry) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    using Smem = WaveSmemT<SHORT>;
+    using Smem = std::conditional_t<PREPASS, WaveSmemPre, WaveSmemT<SHORT>>;
     Smem &sm = reinterpret_cast<Smem *>(smem_raw)[wave];
     constexpr int kPS = Smem::kSteps / 4;              // part rows per channel
 
@@ -146,7 +154,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
             h[1] = __builtin_fmaf(ph.z, h[1], ph.w);
         }
     }
-    float dsum = 0.0f;                                  // sum of dlt over the segment (PREPASS)
+    float dsum = 0.0f;      // PREPASS: this lane's share of the segment's sum of dlt
     const float dskip = p.Dskip ? p.Dskip[dcl] : 0.0f;
     const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
 
@@ -166,9 +174,11 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     const uint32_t seg_n = (uint32_t)(t_end - t_begin);             // a multiple of 16
     const uint32_t act_row = (uint32_t)((dcl - cg * kCh) * L);       // lane's channel row
     // B/C staging: lane (j, q) moves timesteps 4j .. 4j+3 of state rows 2q and
-    // 2q+1 of B and C, i.e. the four entries bc[4j + i][q].
-    const int st_t = 4 * j;
-    const uint32_t bc_row = (uint32_t)(2 * q * L);
+    // 2q+1 of B and C, i.e. the four entries bc[4j + i][q].  The pre-pass swaps
+    // the roles: timesteps 4q .. 4q+3 of B's state rows 2j and 2j+1, i.e. the
+    // entries b2[2q][j] and b2[2q + 1][j].
+    const int st_t = PREPASS ? 4 * q : 4 * j;
+    const uint32_t bc_row = (uint32_t)(2 * (PREPASS ? j : q) * L);
 
     struct Slot { Raw4<IN> u, dl, z, B0, B1, C0, C1; };
     Slot s0, s1;
@@ -192,7 +202,6 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     };
 
     // Phase B step TQ: timesteps 4 TQ .. 4 TQ + 3, operands already in registers.
-    float dsum_chunk = 0.0f;
     auto recur4 = [&](const f32x4 (&ddv)[2], const f32x4 (&bcv)[4], auto tq_c) {
         constexpr int TQ = decltype(tq_c)::value;
         float acc4[4];
@@ -200,21 +209,27 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         for (int k = 0; k < 4; ++k) {
             const float dl = (k & 1) ? ddv[k >> 1].z : ddv[k >> 1].x;
             const float dx = (k & 1) ? ddv[k >> 1].w : ddv[k >> 1].y;
+            const float b0 = PREPASS ? ((k & 1) ? bcv[k >> 1].z : bcv[k >> 1].x) : bcv[k][0];
+            const float b1 = PREPASS ? ((k & 1) ? bcv[k >> 1].w : bcv[k >> 1].y) : bcv[k][1];
             const float a0 = hw_exp2(dl * a2[0]);
             const float a1 = hw_exp2(dl * a2[1]);
-            h[0] = __builtin_fmaf(a0, h[0], dx * bcv[k][0]);
-            h[1] = __builtin_fmaf(a1, h[1], dx * bcv[k][1]);
-            if (PREPASS) dsum_chunk += dl;
-            else acc4[k] = __builtin_fmaf(bcv[k][3], h[1], bcv[k][2] * h[0]);
+            h[0] = __builtin_fmaf(a0, h[0], dx * b0);
+            h[1] = __builtin_fmaf(a1, h[1], dx * b1);
+            if constexpr (!PREPASS) acc4[k] = __builtin_fmaf(bcv[k][3], h[1], bcv[k][2] * h[0]);
         }
-        if (!PREPASS) sm.part[kPS * j + TQ][q] = f32x4{acc4[0], acc4[1], acc4[2], acc4[3]};
+        if constexpr (!PREPASS) sm.part[kPS * j + TQ][q] = f32x4{acc4[0], acc4[1], acc4[2], acc4[3]};
     };
     auto load4 = [&](f32x4 (&ddv)[2], f32x4 (&bcv)[4], auto tq_c) {
         constexpr int TQ = decltype(tq_c)::value;
 #pragma unroll
         for (int k = 0; k < 2; ++k) ddv[k] = sm.dd[2 * TQ + k][j];
+        if constexpr (PREPASS) {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) bcv[k] = sm.bc[4 * TQ + k][q];
+            for (int k = 0; k < 2; ++k) bcv[k] = sm.b2[2 * TQ + k][q];
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) bcv[k] = sm.bc[4 * TQ + k][q];
+        }
     };
     // Order this wave's LDS writes before its later reads of other lanes' data.
     auto wave_sync = [] {
@@ -229,7 +244,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     // phase A has not yet rewritten.  The replay repeats phase B's operations
     // in the same order, so the recorded state equals the one the scan carries.
     auto record_positions = [&](int64_t t0, int nt, float r0, float r1) {
-        for (int64_t k = 0; k < p.npos; ++k) {
+        if constexpr (POS && !PREPASS) for (int64_t k = 0; k < p.npos; ++k) {
             const int64_t pk = p.pos[k * p.batch + b];              // wave-uniform
             if (pk < t0 || pk >= t0 + nt) continue;
             const int cnt = (int)(pk - t0) + 1;
@@ -252,12 +267,13 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         }
     };
 
-    auto store_ck = [&](int64_t t) {                 // the state before timestep t
-        if (live) {
-            float *c = p.ck + ((t / 16) * rows + row) * kN + n0;
-            c[0] = h[0];
-            c[1] = h[1];
-        }
+    // Checkpoints are stored in time order, one per 16 timesteps, so a lane's
+    // pointer steps by one checkpoint plane (rows x kN floats) per store.
+    float *ck_at = CK ? p.ck + ((t_begin / 16) * rows + row) * kN + n0 : nullptr;
+    const int64_t ck_plane = rows * kN;
+    auto store_ck = [&] {                            // the state before the next 16 timesteps
+        if (live) *reinterpret_cast<float2 *>(ck_at) = float2{h[0], h[1]};
+        ck_at += ck_plane;
     };
 
     auto chunk = [&](Slot &sl, int64_t t0) {
@@ -280,12 +296,17 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
                 sm.dd[2 * q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
                 sm.dd[2 * q + 1][j] = f32x4{dl[2], dx[2], dl[3], dx[3]};
             }
+            // pairwise within the quad, then across chunks and lanes: the
+            // rounding of the segment's sum stays small
+            if (PREPASS && 4 * q < nt) dsum += (dl[0] + dl[1]) + (dl[2] + dl[3]);
         }
-        if (!SHORT || j < 4) {
+        if constexpr (PREPASS) {
+            sm.b2[2 * q][j] = f32x4{sl.B0.get(0), sl.B1.get(0), sl.B0.get(1), sl.B1.get(1)};
+            sm.b2[2 * q + 1][j] = f32x4{sl.B0.get(2), sl.B1.get(2), sl.B0.get(3), sl.B1.get(3)};
+        } else if (!SHORT || j < 4) {
 #pragma unroll
             for (int k = 0; k < 4; ++k)
-                sm.bc[st_t + k][q] = PREPASS ? f32x4{sl.B0.get(k), sl.B1.get(k), 0.0f, 0.0f}
-                                             : f32x4{sl.B0.get(k), sl.B1.get(k), sl.C0.get(k), sl.C1.get(k)};
+                sm.bc[st_t + k][q] = f32x4{sl.B0.get(k), sl.B1.get(k), sl.C0.get(k), sl.C1.get(k)};
         }
         wave_sync();
 
@@ -296,7 +317,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         //      step i + 1 are read from LDS while step i computes ----------------
         const float hs0 = POS ? h[0] : 0.0f;        // the state before this chunk
         const float hs1 = POS ? h[1] : 0.0f;
-        if (CK) store_ck(t0);
+        if (CK) store_ck();
         {
             f32x4 ddA[2], bcA[4], ddB[2], bcB[4];
             using I0 = std::integral_constant<int, 0>;
@@ -317,7 +338,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
             if (!SHORT && nt == kT) {
                 load4(ddA, bcA, I4{});
                 recur4(ddB, bcB, I3{});
-                if (CK) store_ck(t0 + 16);
+                if (CK) store_ck();
                 load4(ddB, bcB, I5{});
                 recur4(ddA, bcA, I4{});
                 load4(ddA, bcA, I6{});
@@ -331,37 +352,33 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         }
         wave_sync();
 
-        if (PREPASS) {                              // two-level sum keeps the rounding small
-            dsum += dsum_chunk;
-            dsum_chunk = 0.0f;
-            return;
-        }
-
-        // ---- C: sum the 8 partials of channel j at timesteps 4q .. 4q+3 --------
-        if (4 * q < nt) {
-            f32x4 acc = sm.part[kPS * j + q][0];
+        if constexpr (!PREPASS) {
+            // ---- C: sum the 8 partials of channel j at timesteps 4q .. 4q+3 --------
+            if (4 * q < nt) {
+                f32x4 acc = sm.part[kPS * j + q][0];
 #pragma unroll
-            for (int w = 1; w < kQ; ++w) acc += sm.part[kPS * j + q][w];
-            float yv[4];
+                for (int w = 1; w < kQ; ++w) acc += sm.part[kPS * j + q][w];
+                float yv[4];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                float y = __builtin_fmaf(dskip, xs[k], acc[k]);
-                if (GATE) y *= gs[k];
-                yv[k] = y;
-            }
-            if (live) {
-                const uint32_t oy = act_row + (uint32_t)(t0 - t_begin) + 4 * q;
-                if (OUT == 0) {
-                    *reinterpret_cast<f32x4 *>(yb + oy * 4u) = f32x4{yv[0], yv[1], yv[2], yv[3]};
-                } else {
-                    const uint32_t w0 = (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
-                    const uint32_t w1 = (uint32_t)f32_to_bf16(yv[2]) | ((uint32_t)f32_to_bf16(yv[3]) << 16);
-                    *reinterpret_cast<u32x2 *>(yb + oy * 2u) = u32x2{w0, w1};
+                for (int k = 0; k < 4; ++k) {
+                    float y = __builtin_fmaf(dskip, xs[k], acc[k]);
+                    if (GATE) y *= gs[k];
+                    yv[k] = y;
+                }
+                if (live) {
+                    const uint32_t oy = act_row + (uint32_t)(t0 - t_begin) + 4 * q;
+                    if (OUT == 0) {
+                        *reinterpret_cast<f32x4 *>(yb + oy * 4u) = f32x4{yv[0], yv[1], yv[2], yv[3]};
+                    } else {
+                        const uint32_t w0 = (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
+                        const uint32_t w1 = (uint32_t)f32_to_bf16(yv[2]) | ((uint32_t)f32_to_bf16(yv[3]) << 16);
+                        *reinterpret_cast<u32x2 *>(yb + oy * 2u) = u32x2{w0, w1};
+                    }
                 }
             }
+            if (POS) record_positions(t0, nt, hs0, hs1);
+            wave_sync();   // part / dd / bc are rewritten by the next chunk
         }
-        if (POS) record_positions(t0, nt, hs0, hs1);
-        wave_sync();   // part / dd / bc are rewritten by the next chunk
     };
 
     issue_loads(s0, 0);
@@ -374,7 +391,12 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     if (t0 < t_end) chunk(s0, t0);                  // a full chunk and/or a half chunk remain
     if (t0 + kT < t_end) chunk(s1, t0 + kT);
 
-    if (PREPASS) {
+    if constexpr (PREPASS) {
+        // the eight lanes of channel j hold its timesteps 4q .. 4q+3 of every
+        // chunk: after the butterfly each holds the whole segment's sum
+        dsum += __shfl_xor(dsum, 1);
+        dsum += __shfl_xor(dsum, 2);
+        dsum += __shfl_xor(dsum, 4);
         if (live) {
             const float P0 = hw_exp2(a2[0] * dsum), P1 = hw_exp2(a2[1] * dsum);
             *reinterpret_cast<f32x4 *>(carry + ((seg * rows + row) * kN + n0) * 2) = f32x4{P0, h[0], P1, h[1]};
@@ -388,15 +410,18 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
 // ---- host side: launch configuration -------------------------------------
 
 // Time segments for the tiled path.  One wave covers 8 channels of one batch
-// element.  With fewer than ~0.75 such waves per SIMD (1024 SIMDs) most of the
-// chip idles, so the sequence is cut into segments (each a multiple of 32
-// bytes, at least 256) aiming at about 4 waves per SIMD.  A pre-pass computes
-// each segment's aggregate from a zero state; the scan of segment s then starts
-// from h0 folded with the aggregates of segments 0 .. s-1.  Above that
-// threshold the pre-pass costs more than the extra occupancy returns.
-inline int64_t choose_segments(int64_t waves_base, int64_t L, int64_t *seg_len) {
+// element, and a CU holds two workgroups of the scan at once (its LDS area
+// allows no more): `resident` = 8 waves per CU.  With fewer than 3/8 of that
+// per segment most of the chip idles, so the sequence is cut into segments
+// (each a multiple of 32 bytes, at least 256).  A pre-pass computes each
+// segment's aggregate from a zero state; the scan of segment s then starts
+// from h0 folded with the aggregates of segments 0 .. s-1.  The count is the
+// largest that fills the chip at most twice over: a third round, partly
+// filled, costs more than its shorter segments return.  Above the threshold
+// the pre-pass costs more than the extra occupancy returns.
+inline int64_t choose_segments(int64_t waves_base, int64_t L, int64_t resident, int64_t *seg_len) {
     int64_t nseg = 1;
-    if (waves_base < 768) nseg = (4096 + waves_base - 1) / waves_base;
+    if (waves_base > 0 && waves_base * 8 < resident * 3) nseg = 2 * resident / waves_base;
     const int64_t max_seg = L / 256;
     if (nseg > max_seg) nseg = max_seg;
     if (nseg < 1) nseg = 1;
@@ -406,12 +431,22 @@ inline int64_t choose_segments(int64_t waves_base, int64_t L, int64_t *seg_len) 
     return (L + len - 1) / len;
 }
 
+// Waves of the scan resident at once on the current device (2 workgroups of
+// 4 waves per CU); 256 CUs if the runtime cannot say.
+inline int64_t resident_waves() {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        cus = 256;
+    return 2 * kWavesPerGroup * (int64_t)cus;
+}
+
 template <int IN, int OUT, bool GATE, bool SP>
 hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
     hipStream_t st = static_cast<hipStream_t>(stream);
     const int64_t n_cg = (p.dim + kCh - 1) / kCh;
     int64_t seg_len = p.seqlen;
-    const int64_t nseg = choose_segments(n_cg * p.batch, p.seqlen, &seg_len);
+    const int64_t nseg = p.seqlen >= 512 ? choose_segments(n_cg * p.batch, p.seqlen, resident_waves(), &seg_len) : 1;
     float *carry = nullptr;
     const size_t lds = sizeof(WaveSmem) * kWavesPerGroup;
     hipError_t e;
@@ -423,7 +458,8 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
         const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;
         void *args[] = {&p, &seg_len, &carry};
         e = hipLaunchKernel(reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, true, false>),
-                            dim3((unsigned)blocks), dim3(kThreads), args, lds, st);
+                            dim3((unsigned)blocks), dim3(kThreads), args,
+                            sizeof(WaveSmemPre) * kWavesPerGroup, st);
         if (e != hipSuccess) { (void)hipFreeAsync(carry, st); return e; }
     }
     const int64_t waves = n_cg * p.batch * nseg;
