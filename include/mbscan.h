@@ -198,9 +198,10 @@ int mb_scan_step(int64_t batch, int64_t dim, int64_t dstate,
  *   dDskip, ddt_bias float (D)      required when Dskip / dt_bias are given
  *   dh0       float (B, D, N)       NULL means not written
  * Outputs are overwritten (not accumulated) and must not overlap any other
- * argument; with no row (batch 0) dA, dDskip and ddt_bias are set to zero.  Supported: dstate 16, L a multiple of 16, every activation pointer
- * 16-byte aligned and every float pointer 8-byte aligned (MB_ERR_UNSUPPORTED /
- * MB_ERR_ALIGN otherwise).  Results are deterministic.  The call allocates a
+ * argument; with no row (batch 0) dA, dDskip and ddt_bias are set to zero.
+ * Supported: dstate 16, L a multiple of 16 below 2^25, every activation
+ * pointer 16-byte aligned and every float pointer 8-byte aligned
+ * (MB_ERR_UNSUPPORTED / MB_ERR_ALIGN otherwise).  Results are deterministic.  The call allocates a
  * stream-ordered workspace (hipMallocAsync): state checkpoints every 16 bytes
  * (L/16 x B x D x 16 floats, only when ck is NULL) and per-8-channel dB/dC
  * partials (B x L x D/8 x 64 bytes), freed on the same stream.

@@ -469,7 +469,8 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     const int64_t B = desc->batch, D = desc->dim, L = desc->seqlen, N = desc->dstate;
     if (B < 0 || D < 0 || L < 0 || N < 0) return MB_ERR_SHAPE;
     if (!valid_dtype(desc->in_dtype) || !valid_dtype(desc->out_dtype)) return MB_ERR_DTYPE;
-    if (desc->reserved != 0 || N != 16 || L % 16 != 0) return MB_ERR_UNSUPPORTED;
+    // 32-bit lane offsets inside a wave's rows: (16 rows) x L x 4 bytes < 2^32
+    if (desc->reserved != 0 || N != 16 || L % 16 != 0 || L >= (int64_t(1) << 25)) return MB_ERR_UNSUPPORTED;
     int64_t rows, elems, bc_elems, state_elems;
     if (!mul_ok(B, D, &rows) || !mul_ok(rows, L, &elems) || !mul_ok(B * N, L, &bc_elems) ||
         !mul_ok(rows, N, &state_elems))

@@ -61,31 +61,39 @@ struct BwdParams {
 };
 
 // 2 consecutive activations (4 bytes bf16, 8 bytes fp32).
+// Global addressing: a wave-uniform byte base (the wave's first row) plus a
+// 32-bit lane offset in elements, so that loads and stores take the
+// scalar-base form.  The host keeps L below 2^25, so 16 rows of 4-byte
+// elements stay below 2^32 bytes.
+template <int DT> constexpr uint32_t kElBytes = DT == 1 ? 2u : 4u;
+template <int DT> __device__ __forceinline__ const char *wave_base(const void *p, int64_t el) {
+    return static_cast<const char *>(p) + el * (int64_t)kElBytes<DT>;
+}
+
 template <int DT> struct Raw2;
 template <> struct Raw2<1> {
     uint32_t v;
-    __device__ __forceinline__ void load(const void *base, int64_t off) {
-        v = *reinterpret_cast<const uint32_t *>(static_cast<const uint16_t *>(base) + off);
+    __device__ __forceinline__ void load(const char *base, uint32_t off) {
+        v = *reinterpret_cast<const uint32_t *>(base + off * 2u);
     }
     __device__ __forceinline__ float get(int i) const { return i ? bf16_hi(v) : bf16_lo(v); }
 };
 template <> struct Raw2<0> {
     float v0, v1;
-    __device__ __forceinline__ void load(const void *base, int64_t off) {
-        const float *f = static_cast<const float *>(base) + off;
+    __device__ __forceinline__ void load(const char *base, uint32_t off) {
+        const float *f = reinterpret_cast<const float *>(base + off * 4u);
         v0 = f[0];
         v1 = f[1];
     }
     __device__ __forceinline__ float get(int i) const { return i ? v1 : v0; }
 };
 
-template <int DT> __device__ __forceinline__ void store2(void *base, int64_t off, float a, float b) {
+template <int DT> __device__ __forceinline__ void store2(const char *base, uint32_t off, float a, float b) {
+    char *at = const_cast<char *>(base) + off * kElBytes<DT>;
     if (DT == 0) {
-        *reinterpret_cast<u32x2 *>(static_cast<float *>(base) + off) =
-            u32x2{__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b)};
+        *reinterpret_cast<u32x2 *>(at) = u32x2{__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b)};
     } else {
-        *reinterpret_cast<uint32_t *>(static_cast<uint16_t *>(base) + off) =
-            (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+        *reinterpret_cast<uint32_t *>(at) = (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
     }
 }
 
@@ -194,16 +202,20 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
         a2[s] = p.A[dcl * kN + n0 + s] * kLog2e;
         h[s] = p.h0 ? p.h0[row * kN + n0 + s] : 0.0f;
     }
-    const int64_t act = row * L, bcr = (b * kN + n0) * L;
+    const int64_t row0 = b * p.dim + cg * kCh;          // the wave's first row
+    const uint32_t lrow = (uint32_t)((dcl - cg * kCh) * L), brow = (uint32_t)(n0 * L);
+    const uint32_t lck = (uint32_t)((dcl - cg * kCh) * kN + n0);
+    const char *ub = wave_base<IN>(p.u, row0 * L), *db = wave_base<IN>(p.delta, row0 * L);
+    const char *bb = wave_base<IN>(p.Bm, b * kN * L);
 
     // per element: lane (j, q) takes timesteps 2q, 2q+1; B staging: timesteps 2j, 2j+1
     struct Slot { Raw2<IN> u, dl, b0, b1; };
     auto issue = [&](Slot &sl, int64_t t0) {
-        const int64_t tc = t0 < L ? t0 : L - kT;           // past the end: reload the last chunk
-        sl.u.load(p.u, act + tc + 2 * q);
-        sl.dl.load(p.delta, act + tc + 2 * q);
-        sl.b0.load(p.Bm, bcr + tc + 2 * j);
-        sl.b1.load(p.Bm, bcr + L + tc + 2 * j);
+        const uint32_t tc = (uint32_t)(t0 < L ? t0 : L - kT);   // past the end: reload the last chunk
+        sl.u.load(ub, lrow + tc + 2 * q);
+        sl.dl.load(db, lrow + tc + 2 * q);
+        sl.b0.load(bb, brow + tc + 2 * j);
+        sl.b1.load(bb, brow + (uint32_t)L + tc + 2 * j);
     };
     auto chunk = [&](Slot &sl, int64_t t0) {
 #pragma unroll
@@ -215,7 +227,7 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
         }
         issue(sl, t0 + 2 * kT);
         if (live)
-            *reinterpret_cast<u32x2 *>(p.ck + ((t0 / kT) * rows + row) * kN + n0) =
+            *reinterpret_cast<u32x2 *>(p.ck + ((t0 / kT) * rows + row0) * kN + lck) =
                 u32x2{__builtin_bit_cast(uint32_t, h[0]), __builtin_bit_cast(uint32_t, h[1])};
         wave_sync();
 #pragma unroll
@@ -279,7 +291,15 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
         carry[s] = (p.dh_last && live) ? p.dh_last[row * kN + n0 + s] : 0.0f;   // abar_{t+1} lambda_{t+1}
     }
     float sum_dD = 0.0f, sum_dbias = 0.0f;
-    const int64_t act = row * L, bcr = (b * kN + n0) * L;
+    const int64_t row0 = b * p.dim + cg * kCh;          // the wave's first row
+    const uint32_t lrow = (uint32_t)((dcl - cg * kCh) * L), brow = (uint32_t)(n0 * L);
+    const uint32_t lck = (uint32_t)((dcl - cg * kCh) * kN + n0);
+    const char *ub = wave_base<IN>(p.u, row0 * L), *db = wave_base<IN>(p.delta, row0 * L);
+    const char *zb = GATE ? wave_base<IN>(p.z, row0 * L) : nullptr;
+    const char *bb = wave_base<IN>(p.Bm, b * kN * L), *cb = wave_base<IN>(p.Cm, b * kN * L);
+    const char *dyb = wave_base<OUT>(p.dy, row0 * L);
+    const char *dub = wave_base<OUT>(p.du, row0 * L), *ddb = wave_base<OUT>(p.ddelta, row0 * L);
+    const char *dzb = GATE ? wave_base<OUT>(p.dz, row0 * L) : nullptr;
     float *pbc = p.part_bc + (((WG ? cg / kWaves : cg) * p.batch + b) * L) * (kQ * 4);
     int buf = 0;                                        // WG: the exchange buffer in use
 
@@ -292,15 +312,16 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
     };
     auto issue = [&](Slot &sl, int64_t t0) {
         const int64_t tc = t0 >= 0 ? t0 : 0;
-        sl.u.load(p.u, act + tc + 2 * q);
-        sl.dl.load(p.delta, act + tc + 2 * q);
-        if (GATE) sl.z.load(p.z, act + tc + 2 * q);
-        sl.dy.load(p.dy, act + tc + 2 * q);
-        sl.b0.load(p.Bm, bcr + tc + 2 * j);
-        sl.b1.load(p.Bm, bcr + L + tc + 2 * j);
-        sl.c0.load(p.Cm, bcr + tc + 2 * j);
-        sl.c1.load(p.Cm, bcr + L + tc + 2 * j);
-        const float *ckp = p.ck + ((tc / kT) * rows + row) * kN + n0;
+        const uint32_t oa = lrow + (uint32_t)tc + 2 * q, ob = brow + (uint32_t)tc + 2 * j;
+        sl.u.load(ub, oa);
+        sl.dl.load(db, oa);
+        if (GATE) sl.z.load(zb, oa);
+        sl.dy.load(dyb, oa);
+        sl.b0.load(bb, ob);
+        sl.b1.load(bb, ob + (uint32_t)L);
+        sl.c0.load(cb, ob);
+        sl.c1.load(cb, ob + (uint32_t)L);
+        const float *ckp = p.ck + ((tc / kT) * rows + row0) * kN + lck;
         sl.ck0 = ckp[0];
         sl.ck1 = ckp[1];
     };
@@ -382,7 +403,7 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
                 const float s = __builtin_fmaf(dskip, xs[k], sp[k]);
                 dzv[k] = dyv[k] * s * dsilu[k];
             }
-            if (live) store2<OUT>(p.dz, act + t0 + 2 * q, dzv[0], dzv[1]);
+            if (live) store2<OUT>(dzb, lrow + (uint32_t)t0 + 2 * q, dzv[0], dzv[1]);
         }
         wave_sync();                                    // pa is rewritten below
 
@@ -394,7 +415,7 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
         // the same for b3 = 0 and 1; lanes with b3 = 0 store the even step of a pair,
         // lanes with b3 = 1 the odd one.
         const int b3 = (lane >> 3) & 1;
-        float *const pl = pbc + t0 * (kQ * 4) + b3 * (kQ * 4) + q * 4 + (((lane >> 5) << 1) | ((lane >> 4) & 1));
+        const uint32_t pl = ((uint32_t)t0 + b3) * (kQ * 4) + q * 4 + (((lane >> 5) << 1) | ((lane >> 4) & 1));
 #pragma unroll
         for (int tq = kT / 4 - 1; tq >= 0; --tq) {
             float pu[4], pd[4], tot_hi = 0.0f;
@@ -419,7 +440,7 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
                 } else {                                // steps k, k + 1: b3 = 0 stores k, b3 = 1 stores k + 1
                     const float v = b3 ? tot_hi : tot;
                     if (WG) wg_sums[((buf * kWaves + wave) * 2 + (k >> 1)) * 64 + lane] = v;
-                    else pl[(4 * tq + k) * (kQ * 4)] = v;
+                    else pbc[pl + (4 * tq + k) * (kQ * 4)] = v;
                 }
                 const float u0 = __builtin_fmaf(lam1, bv.y, lam0 * bv.x);
                 const float w0 = lam0 * ab[t][0] * hb[t][0];
@@ -445,7 +466,7 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
                     const float *x0 = wg_sums + (buf * kWaves * 2 + i) * 64 + l;
                     const float sum = (x0[0] + x0[2 * 64]) + (x0[4 * 64] + x0[6 * 64]);
                     const int lslot = ((l >> 5) << 1) | ((l >> 4) & 1);
-                    pbc[(t0 + 4 * tq + 2 * i + ((l >> 3) & 1)) * (kQ * 4) + (l & 7) * 4 + lslot] = sum;
+                    pbc[((uint32_t)t0 + 4 * tq + 2 * i + ((l >> 3) & 1)) * (kQ * 4) + (l & 7) * 4 + lslot] = sum;
                 }
                 buf ^= 1;
             }
@@ -464,8 +485,8 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
                 sum_dbias += ddv[k];
             }
             if (live) {
-                store2<OUT>(p.du, act + t0 + 2 * q, duv[0], duv[1]);
-                store2<OUT>(p.ddelta, act + t0 + 2 * q, ddv[0], ddv[1]);
+                store2<OUT>(dub, lrow + (uint32_t)t0 + 2 * q, duv[0], duv[1]);
+                store2<OUT>(ddb, lrow + (uint32_t)t0 + 2 * q, ddv[0], ddv[1]);
             }
         }
         wave_sync();                                    // dd / bc / pa / pb are rewritten

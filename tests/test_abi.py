@@ -168,6 +168,7 @@ def _bwd(desc, **over):
     (_desc(in_dtype=9), {}, -3),
     (_desc(dstate=8), {}, -5),
     (_desc(seqlen=24), {}, -5),
+    (_desc(seqlen=1 << 25), {}, -5),                    # lane offsets are 32-bit
     (_desc(reserved=1), {}, -5),
     (_desc(), dict(dy=None), -1),
     (_desc(), dict(dA=None), -1),
