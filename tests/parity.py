@@ -9,6 +9,8 @@ import numpy as np
 # reference do not turn rounding noise into an unbounded ratio.
 TOL_Y = 2e-3
 TOL_H = 1e-4
+# y rounded to bf16 on output: the bar plus one bf16 rounding (2^-8 relative)
+TOL_Y_BF16_OUT = TOL_Y + 2.0 ** -8
 
 
 def rel_err(got, ref) -> float:

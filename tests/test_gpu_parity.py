@@ -9,11 +9,11 @@ import pytest
 import torch
 
 from gpu_util import announce, check_against_oracle, gpu_fwd, has_gpu, to_device
+from parity import TOL_Y_BF16_OUT
 from paper_2401_13660_amd.inputs import make_inputs, workload
 
 pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not has_gpu(), reason="needs a GPU")]
 
-BF16_OUT_TOL = 2e-3 + 2.0 ** -8
 
 
 def run_case(inp, **kw):
@@ -59,7 +59,7 @@ def test_one_half_chunk(dtype, gated, softplus, out):
         inp.delta = (np.abs(inp.delta) * np.float32(0.05)).astype(np.float32)
     announce(f"L=16 (5, 100) {dtype} gated={gated} softplus={softplus} out={out}")
     y, h = gpu_fwd(inp, out_dtype=out, delta_softplus=softplus)
-    check_against_oracle(inp, y, h, tol_y=BF16_OUT_TOL if out == torch.bfloat16 else 2e-3,
+    check_against_oracle(inp, y, h, tol_y=TOL_Y_BF16_OUT if out == torch.bfloat16 else 2e-3,
                          delta_softplus=softplus)
 
 
@@ -110,7 +110,7 @@ def test_bf16_output():
     announce("bf16 output (2, 128, 912)")
     y, h = gpu_fwd(inp, out_dtype=torch.bfloat16)
     assert y.dtype == torch.bfloat16
-    check_against_oracle(inp, y, h, tol_y=BF16_OUT_TOL)
+    check_against_oracle(inp, y, h, tol_y=TOL_Y_BF16_OUT)
 
 
 def test_seqlen_zero_returns_h0():
