@@ -65,6 +65,24 @@ template <> struct Raw4<0> {
     __device__ __forceinline__ float get(int i) const { return v[i]; }
 };
 
+// 2 consecutive activations of one row (4 bytes bf16, 8 bytes fp32): the
+// per-lane share of a 16-timestep sequence.
+template <int IN> struct Raw2;
+template <> struct Raw2<1> {
+    uint32_t v;
+    __device__ __forceinline__ void load(const void *base, uint32_t off) {
+        v = *reinterpret_cast<const uint32_t *>(static_cast<const char *>(base) + off * 2u);
+    }
+    __device__ __forceinline__ float get(int i) const { return i ? bf16_hi(v) : bf16_lo(v); }
+};
+template <> struct Raw2<0> {
+    float2 v;
+    __device__ __forceinline__ void load(const void *base, uint32_t off) {
+        v = *reinterpret_cast<const float2 *>(static_cast<const char *>(base) + off * 4u);
+    }
+    __device__ __forceinline__ float get(int i) const { return i ? v.y : v.x; }
+};
+
 // Private LDS area of one wave.  Rows are padded so that both the writes and
 // the reads of every table touch distinct banks (16-byte entries, 64 banks):
 //   dd    row r = timesteps 2r, 2r+1; entry j = (dlt, dx, dlt, dx) of channel j
@@ -78,11 +96,14 @@ constexpr int kPartRow = 9;     // 8 used + 1 pad
 // shape), half the size, so that twice as many waves fit in a CU's LDS.
 template <bool SHORT> struct WaveSmemT {
     static constexpr int kSteps = SHORT ? kT / 2 : kT;
-    f32x4 dd[kSteps / 2][kDdRow];             // 2.25 KB (SHORT: 1.1 KB)
-    f32x4 bc[kSteps][kBcRow];                 // 5 KB (2.5 KB)
-    f32x4 part[kCh * (kSteps / 4)][kPartRow]; // 9 KB (4.5 KB)
+    f32x4 dd[kSteps / 2][kDdRow];                    // 2.25 KB (SHORT: 1.1 KB)
+    f32x4 bc[kSteps][SHORT ? kDdRow : kBcRow];       // 5 KB (SHORT: 2.25 KB, one pad entry
+                                                     // per row, so that 5 workgroups fit in a CU)
+    f32x4 part[kCh * (kSteps / 4)][kPartRow];        // 9 KB (4.5 KB)
 };
 using WaveSmem = WaveSmemT<false>;
+static_assert(sizeof(WaveSmemT<true>) * kWavesPerGroup * 5 <= 160 * 1024,
+              "five workgroups of the 16-timestep tables fit the 160 KB of a CU's LDS");
 // The pre-pass needs neither C nor the output partials.  It stages B two
 // timesteps per entry, and the smaller area lets more waves share a CU:
 //   b2    row r = timesteps 2r, 2r+1; entry q = (B[2q], B[2q+1]) at 2r, then at 2r+1
@@ -103,7 +124,8 @@ struct WaveSmemPre {
 // CK = true (scan only): also store the state at every 16-timestep boundary in
 //   p.ck, the checkpoints the backward recomputes its chunks from.
 // SHORT = true (scan only, seqlen 16): one half chunk per wave, with the
-//   half-size tables of WaveSmemT<true>.
+//   half-size tables of WaveSmemT<true>; phases A and C give every lane two
+//   timesteps (2q, 2q+1) instead of four to half of them.
 template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool PREPASS, bool POS, bool CK = false,
           bool SHORT = false>
 __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len, float *carry) {
@@ -173,25 +195,28 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     char *yb = static_cast<char *>(p.y) + act0 * (OUT == 1 ? 2 : 4);
     const uint32_t seg_n = (uint32_t)(t_end - t_begin);             // a multiple of 16
     const uint32_t act_row = (uint32_t)((dcl - cg * kCh) * L);       // lane's channel row
-    // B/C staging: lane (j, q) moves timesteps 4j .. 4j+3 of state rows 2q and
-    // 2q+1 of B and C, i.e. the four entries bc[4j + i][q].  The pre-pass swaps
-    // the roles: timesteps 4q .. 4q+3 of B's state rows 2j and 2j+1, i.e. the
-    // entries b2[2q][j] and b2[2q + 1][j].
-    const int st_t = PREPASS ? 4 * q : 4 * j;
+    // Elements per lane in phases A and C: timesteps kE q .. kE q + kE - 1.
+    constexpr int kE = SHORT ? 2 : 4;
+    // B/C staging: lane (j, q) moves timesteps kE j .. kE j + kE - 1 of state
+    // rows 2q and 2q+1 of B and C, i.e. the entries bc[kE j + i][q].  The
+    // pre-pass swaps the roles: timesteps 4q .. 4q+3 of B's state rows 2j and
+    // 2j+1, i.e. the entries b2[2q][j] and b2[2q + 1][j].
+    const int st_t = PREPASS ? 4 * q : kE * j;
     const uint32_t bc_row = (uint32_t)(2 * (PREPASS ? j : q) * L);
 
-    struct Slot { Raw4<IN> u, dl, z, B0, B1, C0, C1; };
+    using Raw = std::conditional_t<SHORT, Raw2<IN>, Raw4<IN>>;
+    struct Slot { Raw u, dl, z, B0, B1, C0, C1; };
     Slot s0, s1;
     // Loads never branch: a chunk past the end of the segment reads the last
     // valid quad again (those values are never consumed), so the prefetch
     // registers are written in place every time.
     auto issue_loads = [&](Slot &sl, uint32_t tr) {            // tr: chunk start within the segment
-        const uint32_t ta = tr + 4 * q < seg_n - 4 ? tr + 4 * q : seg_n - 4;
+        const uint32_t ta = tr + kE * q < seg_n - kE ? tr + kE * q : seg_n - kE;
         const uint32_t oa = act_row + ta;
         sl.u.load(ub, oa);
         sl.dl.load(db, oa);
         if (GATE && !PREPASS) sl.z.load(zb, oa);
-        const uint32_t tb = tr + st_t < seg_n - 4 ? tr + st_t : seg_n - 4;
+        const uint32_t tb = tr + st_t < seg_n - kE ? tr + st_t : seg_n - kE;
         const uint32_t ob = bc_row + tb;
         sl.B0.load(bb, ob);
         sl.B1.load(bb, ob + (uint32_t)L);
@@ -279,12 +304,12 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     auto chunk = [&](Slot &sl, int64_t t0) {
         const int nt = SHORT ? kT / 2 : (int)(t_end - t0 < kT ? t_end - t0 : kT);   // multiple of 16
 
-        // ---- A: per-element work of timesteps 4q .. 4q+3 and B/C staging ------
-        float xs[4], gs[4];
+        // ---- A: per-element work of timesteps kE q .. kE q + kE - 1 and B/C staging
+        float xs[kE], gs[kE];
         {
-            float dl[4], dx[4];
+            float dl[kE], dx[kE];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
+            for (int k = 0; k < kE; ++k) {
                 const float x = sl.u.get(k);
                 const float v = sl.dl.get(k) + bias;
                 dl[k] = SOFTPLUS ? softplus_f32(v) : v;
@@ -292,20 +317,22 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
                 xs[k] = x;
                 if (GATE && !PREPASS) gs[k] = silu_f32(sl.z.get(k));
             }
-            if (!SHORT || q < 4) {                  // SHORT: timesteps 16.. do not exist
+            if constexpr (SHORT) {
+                sm.dd[q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
+            } else {
                 sm.dd[2 * q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
                 sm.dd[2 * q + 1][j] = f32x4{dl[2], dx[2], dl[3], dx[3]};
+                // pairwise within the quad, then across chunks and lanes: the
+                // rounding of the segment's sum stays small
+                if (PREPASS && 4 * q < nt) dsum += (dl[0] + dl[1]) + (dl[2] + dl[3]);
             }
-            // pairwise within the quad, then across chunks and lanes: the
-            // rounding of the segment's sum stays small
-            if (PREPASS && 4 * q < nt) dsum += (dl[0] + dl[1]) + (dl[2] + dl[3]);
         }
         if constexpr (PREPASS) {
             sm.b2[2 * q][j] = f32x4{sl.B0.get(0), sl.B1.get(0), sl.B0.get(1), sl.B1.get(1)};
             sm.b2[2 * q + 1][j] = f32x4{sl.B0.get(2), sl.B1.get(2), sl.B0.get(3), sl.B1.get(3)};
-        } else if (!SHORT || j < 4) {
+        } else {
 #pragma unroll
-            for (int k = 0; k < 4; ++k)
+            for (int k = 0; k < kE; ++k)
                 sm.bc[st_t + k][q] = f32x4{sl.B0.get(k), sl.B1.get(k), sl.C0.get(k), sl.C1.get(k)};
         }
         wave_sync();
@@ -353,26 +380,53 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         wave_sync();
 
         if constexpr (!PREPASS) {
-            // ---- C: sum the 8 partials of channel j at timesteps 4q .. 4q+3 --------
-            if (4 * q < nt) {
-                f32x4 acc = sm.part[kPS * j + q][0];
+            // ---- C: sum the 8 partials of channel j at timesteps 2q, 2q+1 ----------
+            if constexpr (SHORT) {
+                // the partials of timesteps 2q, 2q+1 are one half of entry (j, q >> 1)
+                const float2 *src = reinterpret_cast<const float2 *>(&sm.part[kPS * j + (q >> 1)][0]) + (q & 1);
+                float2 acc = src[0];
 #pragma unroll
-                for (int w = 1; w < kQ; ++w) acc += sm.part[kPS * j + q][w];
-                float yv[4];
+                for (int w = 1; w < kQ; ++w) {
+                    acc.x += src[2 * w].x;
+                    acc.y += src[2 * w].y;
+                }
+                float yv[2];
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    float y = __builtin_fmaf(dskip, xs[k], acc[k]);
+                for (int k = 0; k < 2; ++k) {
+                    float y = __builtin_fmaf(dskip, xs[k], k ? acc.y : acc.x);
                     if (GATE) y *= gs[k];
                     yv[k] = y;
                 }
                 if (live) {
-                    const uint32_t oy = act_row + (uint32_t)(t0 - t_begin) + 4 * q;
-                    if (OUT == 0) {
-                        *reinterpret_cast<f32x4 *>(yb + oy * 4u) = f32x4{yv[0], yv[1], yv[2], yv[3]};
-                    } else {
-                        const uint32_t w0 = (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
-                        const uint32_t w1 = (uint32_t)f32_to_bf16(yv[2]) | ((uint32_t)f32_to_bf16(yv[3]) << 16);
-                        *reinterpret_cast<u32x2 *>(yb + oy * 2u) = u32x2{w0, w1};
+                    const uint32_t oy = act_row + (uint32_t)(t0 - t_begin) + 2 * q;
+                    if (OUT == 0)
+                        *reinterpret_cast<float2 *>(yb + oy * 4u) = float2{yv[0], yv[1]};
+                    else
+                        *reinterpret_cast<uint32_t *>(yb + oy * 2u) =
+                            (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
+                }
+            } else {
+                if (4 * q < nt) {
+                    // ---- C: sum the 8 partials of channel j at timesteps 4q .. 4q+3 ----
+                    f32x4 acc = sm.part[kPS * j + q][0];
+#pragma unroll
+                    for (int w = 1; w < kQ; ++w) acc += sm.part[kPS * j + q][w];
+                    float yv[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        float y = __builtin_fmaf(dskip, xs[k], acc[k]);
+                        if (GATE) y *= gs[k];
+                        yv[k] = y;
+                    }
+                    if (live) {
+                        const uint32_t oy = act_row + (uint32_t)(t0 - t_begin) + 4 * q;
+                        if (OUT == 0) {
+                            *reinterpret_cast<f32x4 *>(yb + oy * 4u) = f32x4{yv[0], yv[1], yv[2], yv[3]};
+                        } else {
+                            const uint32_t w0 = (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
+                            const uint32_t w1 = (uint32_t)f32_to_bf16(yv[2]) | ((uint32_t)f32_to_bf16(yv[3]) << 16);
+                            *reinterpret_cast<u32x2 *>(yb + oy * 2u) = u32x2{w0, w1};
+                        }
                     }
                 }
             }
