@@ -20,7 +20,11 @@ namespace {
 using mbs::ScanParams;
 using mbs::StepParams;
 
-constexpr int64_t kMaxElems = int64_t(1) << 62;
+// Every element count the entry points form stays below 2^56, so that byte
+// counts (at most 4 bytes per element, times the position count's factor
+// already inside the count) and the address ranges of the alias checks stay far
+// from overflow.  No device memory comes near it.
+constexpr int64_t kMaxElems = int64_t(1) << 56;
 
 bool valid_dtype(int32_t t) { return t == MB_F32 || t == MB_BF16; }
 size_t dtype_size(int32_t t) { return t == MB_BF16 ? 2 : 4; }
@@ -253,9 +257,9 @@ int scan_fwd_impl(const mb_scan_desc *desc, const void *u, const void *delta, co
     if (B < 0 || D < 0 || L < 0 || N < 0) return MB_ERR_SHAPE;
     if (!valid_dtype(desc->in_dtype) || !valid_dtype(desc->out_dtype)) return MB_ERR_DTYPE;
     if (desc->reserved != 0 || !supported_dstate(N)) return MB_ERR_UNSUPPORTED;
-    int64_t rows, elems, bc_elems, state_elems, pos_elems = 0, hpos_elems = 0;
+    int64_t rows, elems, bn, bc_elems, state_elems, pos_elems = 0, hpos_elems = 0;
     if (npos < 0) return MB_ERR_SHAPE;
-    if (!mul_ok(B, D, &rows) || !mul_ok(rows, L, &elems) || !mul_ok(B * N, L, &bc_elems) ||
+    if (!mul_ok(B, D, &rows) || !mul_ok(rows, L, &elems) || !mul_ok(B, N, &bn) || !mul_ok(bn, L, &bc_elems) ||
         !mul_ok(rows, N, &state_elems) || !mul_ok(npos, B, &pos_elems) ||
         !mul_ok(npos, state_elems, &hpos_elems))
         return MB_ERR_SHAPE;
@@ -471,8 +475,8 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     if (!valid_dtype(desc->in_dtype) || !valid_dtype(desc->out_dtype)) return MB_ERR_DTYPE;
     // 32-bit lane offsets inside a wave's rows: (16 rows) x L x 4 bytes < 2^32
     if (desc->reserved != 0 || N != 16 || L % 16 != 0 || L >= (int64_t(1) << 25)) return MB_ERR_UNSUPPORTED;
-    int64_t rows, elems, bc_elems, state_elems;
-    if (!mul_ok(B, D, &rows) || !mul_ok(rows, L, &elems) || !mul_ok(B * N, L, &bc_elems) ||
+    int64_t rows, elems, bn, bc_elems, state_elems;
+    if (!mul_ok(B, D, &rows) || !mul_ok(rows, L, &elems) || !mul_ok(B, N, &bn) || !mul_ok(bn, L, &bc_elems) ||
         !mul_ok(rows, N, &state_elems))
         return MB_ERR_SHAPE;
     if (L >= (int64_t(1) << 31) || rows >= (int64_t(1) << 31)) return MB_ERR_SHAPE;

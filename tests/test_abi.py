@@ -71,6 +71,7 @@ def _fwd(desc, **over):
     (_desc(batch=-1), {}, -2),
     (_desc(seqlen=-5), {}, -2),
     (_desc(batch=1 << 40, dim=1 << 20, seqlen=1 << 10), {}, -2),
+    (_desc(batch=1 << 61, dim=1, seqlen=16), {}, -2),   # batch x dstate alone past the bound
     (_desc(in_dtype=7), {}, -3),
     (_desc(out_dtype=-1), {}, -3),
     (_desc(dstate=3), {}, -5),
@@ -165,6 +166,7 @@ def _bwd(desc, **over):
 @pytest.mark.parametrize("desc,over,code", [
     (None, {}, -1),
     (_desc(batch=-1), {}, -2),
+    (_desc(batch=1 << 61, dim=1, seqlen=16), {}, -2),
     (_desc(in_dtype=9), {}, -3),
     (_desc(dstate=8), {}, -5),
     (_desc(seqlen=24), {}, -5),
