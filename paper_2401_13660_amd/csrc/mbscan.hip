@@ -169,16 +169,37 @@ hipError_t zero_async(float *p, int64_t n, hipStream_t st) {
 // spans two batch elements) and there are at least 1,536 waves (1.5 per SIMD, so
 // that the other workgroup's waves fill a SIMD while one waits at the
 // workgroup's barrier every 4 steps), the workgroup sums its waves' terms in LDS.
-bool bwd_workgroup_sum(int64_t batch, int64_t dim) {
+bool bwd_workgroup_sum(int64_t batch, int64_t dim, int64_t nseg) {
     namespace W = mbs::bwd;
     const int64_t n_cg = (dim + W::kCh - 1) / W::kCh;
-    return n_cg % W::kWaves == 0 && n_cg * batch >= 1536;
+    return n_cg % W::kWaves == 0 && n_cg * batch * nseg >= 1536;
 }
 
-int64_t bwd_partial_groups(int64_t batch, int64_t dim) {
+int64_t bwd_partial_groups(int64_t batch, int64_t dim, int64_t nseg) {
     namespace W = mbs::bwd;
     const int64_t n_cg = (dim + W::kCh - 1) / W::kCh;
-    return bwd_workgroup_sum(batch, dim) ? n_cg / W::kWaves : n_cg;
+    return bwd_workgroup_sum(batch, dim, nseg) ? n_cg / W::kWaves : n_cg;
+}
+
+// Time segments of the backward.  Its kernel needs up to 256 VGPRs, so 2 waves
+// share a SIMD; with at most half that many 8-channel waves the sequence is cut
+// into the most segments that fill the chip once, each at least 256 bytes and a
+// multiple of 32.  The aggregate pre-pass costs about a quarter of the backward's
+// work per timestep, well below what the extra waves return.
+int64_t bwd_segments(int64_t batch, int64_t dim, int64_t L, int64_t *seg_len) {
+    namespace W = mbs::bwd;
+    const int64_t waves = (dim + W::kCh - 1) / W::kCh * batch;
+    int64_t nseg = 1;
+    if (L >= 512 && waves > 0) {
+        const int64_t resident = mbs::tiled::resident_waves();   // 2 waves per SIMD, as here
+        if (2 * waves <= resident) nseg = resident / waves;
+        if (nseg > L / 256) nseg = L / 256;
+        if (nseg < 1) nseg = 1;
+    }
+    int64_t len = (L + nseg - 1) / nseg;
+    len = (len + 31) / 32 * 32;
+    *seg_len = len;
+    return (L + len - 1) / len;
 }
 
 template <int IN, int OUT, bool GATE, bool SP>
@@ -186,22 +207,30 @@ hipError_t bwd_launch(mbs::bwd::BwdParams &p, bool have_ck, float *dA, float *dB
                       float *dbias, hipStream_t st) {
     namespace W = mbs::bwd;
     const int64_t n_cg = (p.dim + W::kCh - 1) / W::kCh;
+    const int64_t nseg = (p.seqlen + p.seg_len - 1) / p.seg_len;
     const int64_t waves = n_cg * p.batch;
     const dim3 grid((unsigned)((waves + W::kWaves - 1) / W::kWaves)), block(W::kThreads);
+    const dim3 grid_seg((unsigned)((waves * nseg + W::kWaves - 1) / W::kWaves));
     const size_t lds = sizeof(W::WaveSmem) * W::kWaves;
     void *args[] = {&p};
     hipError_t e = hipSuccess;
     if (!have_ck)
         e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_ckpt<IN, SP>), grid, block, args, lds, st);
     if (e != hipSuccess) return e;
-    if (bwd_workgroup_sum(p.batch, p.dim))
-        e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_bwd<IN, OUT, GATE, SP, true>), grid, block,
-                            args, lds, st);                      // + its static exchange area
+    if (nseg > 1) {
+        const dim3 grid_agg((unsigned)((waves * (nseg - 1) + W::kWaves - 1) / W::kWaves));
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&W::bwd_seg_aggregate<IN, OUT, GATE, SP>), grid_agg,
+                            block, args, sizeof(W::AggSmem) * W::kWaves, st);
+        if (e != hipSuccess) return e;
+    }
+    if (bwd_workgroup_sum(p.batch, p.dim, nseg))
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_bwd<IN, OUT, GATE, SP, true>), grid_seg,
+                            block, args, lds, st);               // + its static exchange area
     else
-        e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_bwd<IN, OUT, GATE, SP, false>), grid, block,
-                            args, lds, st);
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_bwd<IN, OUT, GATE, SP, false>), grid_seg,
+                            block, args, lds, st);
     if (e != hipSuccess) return e;
-    int64_t ncg = bwd_partial_groups(p.batch, p.dim);
+    int64_t ncg = bwd_partial_groups(p.batch, p.dim, nseg);
     void *fargs[] = {&p, &dB, &dC, &ncg};
     const int64_t nbc = p.batch * p.seqlen * W::kQ;
     e = hipLaunchKernel(reinterpret_cast<const void *>(&W::bwd_finish_bc), dim3((unsigned)((nbc + 255) / 256)),
@@ -540,12 +569,15 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     }
 
     namespace W = mbs::bwd;
-    const int64_t n_cg = bwd_partial_groups(B, D);       // dB/dC partials per (batch, t)
+    int64_t seg_len = L;
+    const int64_t nseg = bwd_segments(B, D, L, &seg_len);
+    const int64_t n_cg = bwd_partial_groups(B, D, nseg);       // dB/dC partials per (batch, t)
     const size_t ck_b = ck ? 0 : (size_t)(L / W::kT) * (size_t)rows * W::kN * 4;
     const size_t bcp_b = (size_t)n_cg * (size_t)B * (size_t)L * W::kQ * 4 * 4;
-    const size_t row_b = (size_t)rows * (W::kN + 2) * 4;
+    const size_t row_b = (size_t)nseg * (size_t)rows * (W::kN + 2) * 4;
+    const size_t agg_b = nseg > 1 ? (size_t)nseg * (size_t)rows * W::kN * 2 * 4 : 0;
     char *ws = nullptr;
-    e = hipMallocAsync(reinterpret_cast<void **>(&ws), ck_b + bcp_b + row_b, st);
+    e = hipMallocAsync(reinterpret_cast<void **>(&ws), ck_b + bcp_b + row_b + agg_b, st);
     if (e != hipSuccess) return MB_ERR_HIP;
     W::BwdParams p{};
     p.batch = B; p.dim = D; p.seqlen = L;
@@ -556,6 +588,8 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     p.ck = ck ? const_cast<float *>(ck) : reinterpret_cast<float *>(ws);   // given: read only
     p.part_bc = reinterpret_cast<float *>(ws + ck_b);
     p.part_row = reinterpret_cast<float *>(ws + ck_b + bcp_b);
+    p.seg_len = seg_len;
+    p.agg = nseg > 1 ? reinterpret_cast<float *>(ws + ck_b + bcp_b + row_b) : nullptr;
     p.delta_softplus = desc->delta_softplus ? 1 : 0;
     float *dD = Dskip ? dDskip : nullptr, *dbias = dt_bias ? ddt_bias : nullptr;
     if (desc->in_dtype == MB_F32)

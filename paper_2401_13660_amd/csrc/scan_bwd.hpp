@@ -24,7 +24,12 @@
 //               (C2).  dB and dC are summed over the wave's 8 channels in
 //               registers (lane swaps) and written as one partial per wave;
 //   bwd_finish  sums the dB / dC partials over channel groups and dA, dDskip,
-//               dbias over the batch (no atomics: results are deterministic).
+//               dbias over the batch and the time segments (no atomics: results
+//               are deterministic).
+// With few (batch, channel) rows, time is cut into segments so that more waves
+// share the chip: bwd_seg_aggregate runs the adjoint recurrence of every segment
+// but the first from a zero carry, and the wave of segment s starts from
+// dh_last folded with the aggregates of the segments after it.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -56,7 +61,14 @@ struct BwdParams {
     float *ck;                         // (L / 16, batch * dim, 16) checkpoints
     float *part_bc;                    // (ncg, batch, L, 8, 4): per wave, summed over its channels:
                                        // (dB[2q], dC[2q], dB[2q+1], dC[2q+1]) of state pair q
-    float *part_row;                   // (batch * dim, 16 + 2): dA (16), dDskip, dbias per row
+    float *part_row;                   // (nseg, batch * dim, 16 + 2): dA (16), dDskip, dbias per row
+                                       // and time segment
+    // Time segments (few rows): segment s covers [s seg_len, (s + 1) seg_len) of L.
+    // agg[((s * rows + row) * 16 + n) * 2 + {0, 1}] = (P, H) of segment s >= 1: the
+    // carry abar_{t_b} lambda_{t_b} it hands to segment s - 1 is P c + H, for the
+    // carry c = abar_{t_e} lambda_{t_e} that enters its last timestep.
+    int64_t seg_len;
+    float *agg;
     int delta_softplus;
 };
 
@@ -257,6 +269,105 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
     if (t0 < L) chunk(s0, t0);
 }
 
+// ---- the adjoint aggregate of a time segment ---------------------------------------
+// The adjoint recurrence is linear in its carry: within [t_b, t_e),
+// lambda_t = ds_t C_t + carry and the next carry is abar_t lambda_t, so the carry
+// handed on, abar_{t_b} lambda_{t_b}, is P c + H for the carry c entering t_e - 1,
+// with P = prod_t abar_t = 2^(A log2 e sum_t dlt_t) and H the carry from c = 0.
+// (The associative operator of Section 2 applied to the adjoint, backwards.)
+// Lanes own channel j, states 2q, 2q+1 as in scan_bwd; per 16-step chunk the
+// wave stages (dlt, ds) and C, then runs the recurrence backwards.
+struct AggSmem {
+    float2 dd[kT][kCh + 1];           // (dlt, ds) of timestep t, channel j
+    float2 cc[kT][kQ + 1];            // (C[2q], C[2q+1]) at timestep t
+};
+
+template <int IN, int OUT, bool GATE, bool SOFTPLUS>
+__global__ __launch_bounds__(kThreads) void bwd_seg_aggregate(BwdParams p) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    AggSmem &sm = reinterpret_cast<AggSmem *>(smem_raw)[__builtin_amdgcn_readfirstlane(threadIdx.x >> 6)];
+    const int lane = threadIdx.x & 63, j = lane >> 3, q = lane & 7, n0 = 2 * q;
+    const int64_t n_cg = (p.dim + kCh - 1) / kCh, L = p.seqlen;
+    const int64_t nseg = (L + p.seg_len - 1) / p.seg_len;
+    const int64_t wid = wave_id();
+    if (wid >= n_cg * p.batch * (nseg - 1)) return;    // segments 1 .. nseg-1
+    const int64_t cg = wid % n_cg, b = (wid / n_cg) % p.batch, seg = 1 + wid / (n_cg * p.batch);
+    const int64_t t_begin = seg * p.seg_len;
+    const int64_t t_end = t_begin + p.seg_len < L ? t_begin + p.seg_len : L;
+    const int64_t d = cg * kCh + j;
+    const bool live = d < p.dim;
+    const int64_t dcl = live ? d : p.dim - 1;
+    const int64_t row = b * p.dim + dcl, rows = p.batch * p.dim;
+    const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
+    float a2[2], carry[2] = {0.0f, 0.0f}, dsum = 0.0f;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) a2[s] = p.A[dcl * kN + n0 + s] * kLog2e;
+    const int64_t row0 = b * p.dim + cg * kCh;
+    const uint32_t lrow = (uint32_t)((dcl - cg * kCh) * L), brow = (uint32_t)(n0 * L);
+    const char *db = wave_base<IN>(p.delta, row0 * L);
+    const char *zb = GATE ? wave_base<IN>(p.z, row0 * L) : nullptr;
+    const char *cb = wave_base<IN>(p.Cm, b * kN * L);
+    const char *dyb = wave_base<OUT>(p.dy, row0 * L);
+
+    // per element: lane (j, q) takes timesteps 2q, 2q+1; C staging: timesteps 2j, 2j+1
+    struct Slot { Raw2<IN> dl, z, c0, c1; Raw2<OUT> dy; };
+    auto issue = [&](Slot &sl, int64_t t0) {                // clamped at the segment start
+        const uint32_t tc = (uint32_t)(t0 >= t_begin ? t0 : t_begin);
+        const uint32_t oa = lrow + tc + 2 * q, ob = brow + tc + 2 * j;
+        sl.dl.load(db, oa);
+        if (GATE) sl.z.load(zb, oa);
+        sl.dy.load(dyb, oa);
+        sl.c0.load(cb, ob);
+        sl.c1.load(cb, ob + (uint32_t)L);
+    };
+    auto chunk = [&](Slot &sl, int64_t t0) {
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const float v = sl.dl.get(k) + bias;
+            const float dl = SOFTPLUS ? softplus_f32(v) : v;
+            const float g = GATE ? silu_f32(sl.z.get(k)) : 1.0f;
+            dsum += dl;
+            // a dead lane has ds = 0, so its carry stays exactly 0
+            sm.dd[2 * q + k][j] = float2{dl, live ? sl.dy.get(k) * g : 0.0f};
+            sm.cc[2 * j + k][q] = float2{sl.c0.get(k), sl.c1.get(k)};
+        }
+        wave_sync();
+        issue(sl, t0 - 2 * kT);                          // the chunk two further back
+#pragma unroll
+        for (int t = kT - 1; t >= 0; --t) {
+            const float2 dv = sm.dd[t][j];
+            const float2 cv = sm.cc[t][q];
+            const float lam0 = __builtin_fmaf(dv.y, cv.x, carry[0]);
+            const float lam1 = __builtin_fmaf(dv.y, cv.y, carry[1]);
+            carry[0] = hw_exp2(dv.x * a2[0]) * lam0;
+            carry[1] = hw_exp2(dv.x * a2[1]) * lam1;
+        }
+        wave_sync();                                     // dd / cc are rewritten
+    };
+
+    Slot s0, s1;
+    issue(s0, t_end - kT);
+    issue(s1, t_end - 2 * kT);
+    int64_t t0 = t_end - kT;
+    for (; t0 - kT >= t_begin; t0 -= 2 * kT) {
+        chunk(s0, t0);
+        chunk(s1, t0 - kT);
+    }
+    if (t0 >= t_begin) chunk(s0, t0);
+
+    dsum += __shfl_xor(dsum, 1);                         // the segment's sum of dlt for channel j
+    dsum += __shfl_xor(dsum, 2);
+    dsum += __shfl_xor(dsum, 4);
+    if (live) {
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+            float *o = p.agg + ((seg * rows + row) * kN + n0 + s) * 2;
+            o[0] = hw_exp2(a2[s] * dsum);
+            o[1] = carry[s];
+        }
+    }
+}
+
 // ---- the backward pass -----------------------------------------------------------
 // Floats of the workgroup's dB/dC exchange area (WG = true): two buffers of
 // 4 waves x 2 step pairs x 64 lanes.
@@ -273,14 +384,17 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     WaveSmem &sm = reinterpret_cast<WaveSmem *>(smem_raw)[wave];
     const int lane = threadIdx.x & 63, j = lane >> 3, q = lane & 7, n0 = 2 * q;
-    const int64_t n_cg = (p.dim + kCh - 1) / kCh;
+    const int64_t n_cg = (p.dim + kCh - 1) / kCh, L = p.seqlen;
+    const int64_t nseg = (L + p.seg_len - 1) / p.seg_len;
     const int64_t wid = wave_id();
-    if (wid >= n_cg * p.batch) return;
-    const int64_t cg = wid % n_cg, b = wid / n_cg;
+    if (wid >= n_cg * p.batch * nseg) return;
+    const int64_t cg = wid % n_cg, b = (wid / n_cg) % p.batch, seg = wid / (n_cg * p.batch);
+    const int64_t t_begin = seg * p.seg_len;
+    const int64_t t_end = t_begin + p.seg_len < L ? t_begin + p.seg_len : L;
     const int64_t d = cg * kCh + j;
     const bool live = d < p.dim;
     const int64_t dcl = live ? d : p.dim - 1;
-    const int64_t row = b * p.dim + dcl, rows = p.batch * p.dim, L = p.seqlen;
+    const int64_t row = b * p.dim + dcl, rows = p.batch * p.dim;
     const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
     const float dskip = p.Dskip ? p.Dskip[dcl] : 0.0f;
     float a2[2], Av[2], carry[2], dA[2] = {0.0f, 0.0f};
@@ -289,6 +403,11 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
         Av[s] = p.A[dcl * kN + n0 + s];
         a2[s] = Av[s] * kLog2e;
         carry[s] = (p.dh_last && live) ? p.dh_last[row * kN + n0 + s] : 0.0f;   // abar_{t+1} lambda_{t+1}
+        // carry-in: fold the aggregates of the later segments, the last one first
+        for (int64_t s2 = nseg - 1; s2 > seg; --s2) {
+            const float *a = p.agg + ((s2 * rows + row) * kN + n0 + s) * 2;
+            carry[s] = live ? __builtin_fmaf(a[0], carry[s], a[1]) : 0.0f;
+        }
     }
     float sum_dD = 0.0f, sum_dbias = 0.0f;
     const int64_t row0 = b * p.dim + cg * kCh;          // the wave's first row
@@ -304,14 +423,14 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
     int buf = 0;                                        // WG: the exchange buffer in use
 
     // Loads run two chunks ahead (in processing order: backwards in time) in two
-    // static register slots, clamped at the sequence start, never branched.
+    // static register slots, clamped at the segment start, never branched.
     struct Slot {
         Raw2<IN> u, dl, z, b0, b1, c0, c1;
         Raw2<OUT> dy;
         float ck0, ck1;
     };
     auto issue = [&](Slot &sl, int64_t t0) {
-        const int64_t tc = t0 >= 0 ? t0 : 0;
+        const int64_t tc = t0 >= t_begin ? t0 : t_begin;
         const uint32_t oa = lrow + (uint32_t)tc + 2 * q, ob = brow + (uint32_t)tc + 2 * j;
         sl.u.load(ub, oa);
         sl.dl.load(db, oa);
@@ -493,14 +612,14 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
     };
 
     Slot s0, s1;
-    issue(s0, L - kT);
-    issue(s1, L - 2 * kT);
-    int64_t t0 = L - kT;
-    for (; t0 - kT >= 0; t0 -= 2 * kT) {               // pairs of chunks, backwards
+    issue(s0, t_end - kT);
+    issue(s1, t_end - 2 * kT);
+    int64_t t0 = t_end - kT;
+    for (; t0 - kT >= t_begin; t0 -= 2 * kT) {         // pairs of chunks, backwards
         chunk(s0, t0);
         chunk(s1, t0 - kT);
     }
-    if (t0 >= 0) chunk(s0, t0);
+    if (t0 >= t_begin) chunk(s0, t0);
 
     // ---- per-row results: dh0, dA (per state), dDskip and dbias (per channel) ----
 #pragma unroll
@@ -509,11 +628,11 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
         sum_dbias += __shfl_xor(sum_dbias, off, 64);
     }
     if (live) {
-        if (p.dh0) {
+        if (p.dh0 && seg == 0) {
             p.dh0[row * kN + n0] = carry[0];
             p.dh0[row * kN + n0 + 1] = carry[1];
         }
-        float *pr = p.part_row + row * (kN + 2);
+        float *pr = p.part_row + (seg * rows + row) * (kN + 2);
         pr[n0] = dA[0];
         pr[n0 + 1] = dA[1];
         if (q == 0) {
@@ -541,13 +660,17 @@ __global__ __launch_bounds__(256) void bwd_finish_bc(BwdParams p, float *dB, flo
     dC[(b * kN + n0 + 1) * L + t] = sum.w;
 }
 
-// dA[d][n], dDskip[d], dbias[d]: thread (d, slot) sums over the batch.
+// dA[d][n], dDskip[d], dbias[d]: thread (d, slot) sums over the batch and the
+// time segments.
 __global__ __launch_bounds__(256) void bwd_finish_rows(BwdParams p, float *dA, float *dD, float *dbias) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;   // (d, slot)
     if (i >= p.dim * (kN + 2)) return;
     const int64_t d = i / (kN + 2), slot = i % (kN + 2);
+    const int64_t nseg = (p.seqlen + p.seg_len - 1) / p.seg_len;
     float sum = 0.0f;
-    for (int64_t b = 0; b < p.batch; ++b) sum += p.part_row[(b * p.dim + d) * (kN + 2) + slot];
+    for (int64_t s = 0; s < nseg; ++s)
+        for (int64_t b = 0; b < p.batch; ++b)
+            sum += p.part_row[((s * p.batch + b) * p.dim + d) * (kN + 2) + slot];
     if (slot < kN) dA[d * kN + slot] = sum;
     else if (slot == kN) { if (dD) dD[d] = sum; }
     else if (dbias) dbias[d] = sum;
