@@ -67,9 +67,12 @@ def grads_case(inp, *, with_dhl=True, out_dtype=torch.float32, delta_softplus=Tr
 # 8-channel group; a long reverse carry; a single ragged group; one group; more
 # than 1,024 channel groups (more waves than SIMDs), with and without dead lanes;
 # at least 1,536 groups, a multiple of 4 per batch element, where the 4 waves of a
-# workgroup also sum their dB/dC terms with each other, with and without dead lanes.
+# workgroup also sum their dB/dC terms with each other, with and without dead lanes;
+# few rows and a long sequence, cut into time segments (3 segments, the last one
+# shorter; 8 segments whose waves also take the workgroup sum).
 @pytest.mark.parametrize("shape", [(2, 196, 16), (3, 101, 48), (2, 197, 1008), (1, 5, 32), (1, 8, 16),
-                                   (9, 1001, 32), (9, 1024, 16), (12, 1024, 16), (12, 1020, 32)])
+                                   (9, 1001, 32), (9, 1024, 16), (12, 1024, 16), (12, 1020, 32),
+                                   (2, 1024, 2048)])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_bwd_shapes(shape, dtype):
     inp = make_inputs(*shape, 16, dtype=dtype, seed=61, with_h0=True)
@@ -125,8 +128,8 @@ def test_bwd_empty_sequence():
     assert torch.count_nonzero(g0["dA"]) == 0, "dA over an empty batch must be zero"
 
 
-@pytest.mark.parametrize("shape", [(2, 128, 512), (9, 1001, 64), (12, 1020, 64)],
-                         ids=["small", "many_groups", "workgroup_sum"])
+@pytest.mark.parametrize("shape", [(2, 128, 512), (9, 1001, 64), (12, 1020, 64), (2, 1024, 2048)],
+                         ids=["small_two_segments", "many_groups", "workgroup_sum", "segments_and_workgroup_sum"])
 def test_bwd_deterministic(shape):
     import paper_2401_13660_amd as mb
     inp = make_inputs(*shape, 16, dtype="bf16", seed=65, with_h0=True)
