@@ -208,14 +208,34 @@ hipError_t bwd_launch(mbs::bwd::BwdParams &p, bool have_ck, float *dA, float *dB
     namespace W = mbs::bwd;
     const int64_t n_cg = (p.dim + W::kCh - 1) / W::kCh;
     const int64_t nseg = (p.seqlen + p.seg_len - 1) / p.seg_len;
+    const int64_t ck_nseg = (p.seqlen + p.ck_seg_len - 1) / p.ck_seg_len;
     const int64_t waves = n_cg * p.batch;
     const dim3 grid((unsigned)((waves + W::kWaves - 1) / W::kWaves)), block(W::kThreads);
     const dim3 grid_seg((unsigned)((waves * nseg + W::kWaves - 1) / W::kWaves));
     const size_t lds = sizeof(W::WaveSmem) * W::kWaves;
     void *args[] = {&p};
     hipError_t e = hipSuccess;
-    if (!have_ck)
-        e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_ckpt<IN, SP>), grid, block, args, lds, st);
+    if (!have_ck && ck_nseg > 1) {
+        // the forward pre-pass: each segment's state aggregate, for scan_ckpt's carry-in
+        mbs::ScanParams f{};
+        f.batch = p.batch; f.dim = p.dim; f.seqlen = p.seqlen;
+        f.u = p.u; f.delta = p.delta; f.Bm = p.Bm; f.Cm = p.Cm;
+        f.A = p.A; f.dt_bias = p.dt_bias;
+        f.y = p.du;                                      // never written by the pre-pass
+        f.delta_softplus = p.delta_softplus;
+        int64_t seg_len = p.ck_seg_len;
+        float *fagg = const_cast<float *>(p.fagg);
+        void *fargs[] = {&f, &seg_len, &fagg};
+        namespace T = mbs::tiled;
+        const dim3 grid_pre((unsigned)((waves * (ck_nseg - 1) + T::kWavesPerGroup - 1) / T::kWavesPerGroup));
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&T::scan_fwd_tiled<IN, 0, false, SP, true, false>),
+                            grid_pre, dim3(T::kThreads), fargs, sizeof(T::WaveSmemPre) * T::kWavesPerGroup, st);
+        if (e != hipSuccess) return e;
+    }
+    if (!have_ck) {
+        const dim3 grid_ck((unsigned)((waves * ck_nseg + W::kWaves - 1) / W::kWaves));
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&W::scan_ckpt<IN, SP>), grid_ck, block, args, lds, st);
+    }
     if (e != hipSuccess) return e;
     if (nseg > 1) {
         const dim3 grid_agg((unsigned)((waves * (nseg - 1) + W::kWaves - 1) / W::kWaves));
@@ -576,8 +596,13 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     const size_t bcp_b = (size_t)n_cg * (size_t)B * (size_t)L * W::kQ * 4 * 4;
     const size_t row_b = (size_t)nseg * (size_t)rows * (W::kN + 2) * 4;
     const size_t agg_b = nseg > 1 ? (size_t)nseg * (size_t)rows * W::kN * 2 * 4 : 0;
+    // The checkpoint pass is a forward recurrence: its pre-pass costs as much per
+    // timestep as the pass itself, so it takes the segments only with at most a
+    // third as many waves as the chip holds.
+    const int64_t ck_nseg = (!ck && 3 * ((D + W::kCh - 1) / W::kCh * B) <= mbs::tiled::resident_waves()) ? nseg : 1;
+    const size_t fagg_b = ck_nseg > 1 ? (size_t)(ck_nseg - 1) * (size_t)rows * W::kN * 2 * 4 : 0;
     char *ws = nullptr;
-    e = hipMallocAsync(reinterpret_cast<void **>(&ws), ck_b + bcp_b + row_b + agg_b, st);
+    e = hipMallocAsync(reinterpret_cast<void **>(&ws), ck_b + bcp_b + row_b + agg_b + fagg_b, st);
     if (e != hipSuccess) return MB_ERR_HIP;
     W::BwdParams p{};
     p.batch = B; p.dim = D; p.seqlen = L;
@@ -589,7 +614,9 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     p.part_bc = reinterpret_cast<float *>(ws + ck_b);
     p.part_row = reinterpret_cast<float *>(ws + ck_b + bcp_b);
     p.seg_len = seg_len;
+    p.ck_seg_len = ck_nseg > 1 ? seg_len : (L + 31) / 32 * 32;
     p.agg = nseg > 1 ? reinterpret_cast<float *>(ws + ck_b + bcp_b + row_b) : nullptr;
+    p.fagg = fagg_b ? reinterpret_cast<float *>(ws + ck_b + bcp_b + row_b + agg_b) : nullptr;
     p.delta_softplus = desc->delta_softplus ? 1 : 0;
     float *dD = Dskip ? dDskip : nullptr, *dbias = dt_bias ? ddt_bias : nullptr;
     if (desc->in_dtype == MB_F32)

@@ -67,8 +67,14 @@ struct BwdParams {
     // agg[((s * rows + row) * 16 + n) * 2 + {0, 1}] = (P, H) of segment s >= 1: the
     // carry abar_{t_b} lambda_{t_b} it hands to segment s - 1 is P c + H, for the
     // carry c = abar_{t_e} lambda_{t_e} that enters its last timestep.
+    // scan_ckpt's own segments, of ck_seg_len (>= L: none):
+    // fagg[((s * rows + row) * 16 + n) * 2 + {0, 1}] = the forward aggregate (P, H)
+    // of its segment s < nseg - 1 (the forward pre-pass's layout); it starts
+    // segment s from h0 folded with those of segments 0 .. s-1.
     int64_t seg_len;
     float *agg;
+    int64_t ck_seg_len;
+    const float *fagg;
     int delta_softplus;
 };
 
@@ -199,20 +205,27 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     WaveSmem &sm = reinterpret_cast<WaveSmem *>(smem_raw)[__builtin_amdgcn_readfirstlane(threadIdx.x >> 6)];
     const int lane = threadIdx.x & 63, j = lane >> 3, q = lane & 7, n0 = 2 * q;
-    const int64_t n_cg = (p.dim + kCh - 1) / kCh;
+    const int64_t n_cg = (p.dim + kCh - 1) / kCh, L = p.seqlen;
+    const int64_t nseg = (L + p.ck_seg_len - 1) / p.ck_seg_len;
     const int64_t wid = wave_id();
-    if (wid >= n_cg * p.batch) return;
-    const int64_t cg = wid % n_cg, b = wid / n_cg;
+    if (wid >= n_cg * p.batch * nseg) return;
+    const int64_t cg = wid % n_cg, b = (wid / n_cg) % p.batch, seg = wid / (n_cg * p.batch);
+    const int64_t t_begin = seg * p.ck_seg_len;
+    const int64_t t_end = t_begin + p.ck_seg_len < L ? t_begin + p.ck_seg_len : L;
     const int64_t d = cg * kCh + j;
     const bool live = d < p.dim;
     const int64_t dcl = live ? d : p.dim - 1;
-    const int64_t row = b * p.dim + dcl, rows = p.batch * p.dim, L = p.seqlen;
+    const int64_t row = b * p.dim + dcl, rows = p.batch * p.dim;
     const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
     float a2[2], h[2];
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
         a2[s] = p.A[dcl * kN + n0 + s] * kLog2e;
         h[s] = p.h0 ? p.h0[row * kN + n0 + s] : 0.0f;
+        for (int64_t s2 = 0; s2 < seg; ++s2) {           // carry-in of the earlier segments
+            const float *f = p.fagg + ((s2 * rows + row) * kN + n0 + s) * 2;
+            h[s] = __builtin_fmaf(f[0], h[s], f[1]);
+        }
     }
     const int64_t row0 = b * p.dim + cg * kCh;          // the wave's first row
     const uint32_t lrow = (uint32_t)((dcl - cg * kCh) * L), brow = (uint32_t)(n0 * L);
@@ -223,7 +236,7 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
     // per element: lane (j, q) takes timesteps 2q, 2q+1; B staging: timesteps 2j, 2j+1
     struct Slot { Raw2<IN> u, dl, b0, b1; };
     auto issue = [&](Slot &sl, int64_t t0) {
-        const uint32_t tc = (uint32_t)(t0 < L ? t0 : L - kT);   // past the end: reload the last chunk
+        const uint32_t tc = (uint32_t)(t0 < t_end ? t0 : t_end - kT);   // past the end: reload the last chunk
         sl.u.load(ub, lrow + tc + 2 * q);
         sl.dl.load(db, lrow + tc + 2 * q);
         sl.b0.load(bb, brow + tc + 2 * j);
@@ -259,14 +272,14 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
         wave_sync();
     };
     Slot s0, s1;
-    issue(s0, 0);
-    issue(s1, kT);
-    int64_t t0 = 0;
-    for (; t0 + 2 * kT <= L; t0 += 2 * kT) {
+    issue(s0, t_begin);
+    issue(s1, t_begin + kT);
+    int64_t t0 = t_begin;
+    for (; t0 + 2 * kT <= t_end; t0 += 2 * kT) {
         chunk(s0, t0);
         chunk(s1, t0 + kT);
     }
-    if (t0 < L) chunk(s0, t0);
+    if (t0 < t_end) chunk(s0, t0);
 }
 
 // ---- the adjoint aggregate of a time segment ---------------------------------------
