@@ -24,20 +24,37 @@ __global__ __launch_bounds__(256) void scan_step_kernel(StepParams p) {
     const int64_t b = r / p.dim;
     const int64_t d = r - b * p.dim;
 
-    const float x = Act<IN>::ld(p.u, r);
-    const float v = Act<IN>::ld(p.delta, r) + (p.dt_bias ? p.dt_bias[d] : 0.0f);
-    const float dlt = p.delta_softplus ? softplus_f32(v) : v;
-    const float dx = dlt * x;
-
-    float acc = 0.0f;
-    float hs[S];
+    // Every load is issued before the first use of any of them, so that a step
+    // costs one round trip to memory instead of three (activations, then state,
+    // then gate).  An absent optional input reads a stand-in of the same size
+    // (u for z, A for Dskip and dt_bias) and its value is discarded, so no load
+    // sits in a branch that would wait for it.  The 4 lanes of a row read the
+    // same activation words.
+    float hs[S], av[S], bv[S], cv[S];
 #pragma unroll
     for (int s = 0; s < S; ++s) {
         const int n = part * S + s;
-        const float abar = hw_exp2(dlt * (p.A[d * N + n] * kLog2e));
-        const float bx = dx * Act<IN>::ld(p.Bt, b * N + n);
-        hs[s] = __builtin_fmaf(abar, p.h[r * N + n], bx);
-        acc = __builtin_fmaf(Act<IN>::ld(p.Ct, b * N + n), hs[s], acc);
+        hs[s] = p.h[r * N + n];
+        av[s] = p.A[d * N + n];
+        bv[s] = Act<IN>::ld(p.Bt, b * N + n);
+        cv[s] = Act<IN>::ld(p.Ct, b * N + n);
+    }
+    const float x = Act<IN>::ld(p.u, r);
+    const float draw = Act<IN>::ld(p.delta, r);
+    const float bias_raw = (p.dt_bias ? p.dt_bias : p.A)[d];
+    const float z_raw = Act<IN>::ld(p.z ? p.z : p.u, r);
+    const float dskip_raw = (p.Dskip ? p.Dskip : p.A)[d];
+    const float bias = p.dt_bias ? bias_raw : 0.0f;
+    const float dskip = p.Dskip ? dskip_raw : 0.0f;
+    const float v = draw + bias;
+    const float dlt = p.delta_softplus ? softplus_f32(v) : v;
+    const float dx = dlt * x;
+    float acc = 0.0f;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        const float abar = hw_exp2(dlt * (av[s] * kLog2e));
+        hs[s] = __builtin_fmaf(abar, hs[s], dx * bv[s]);
+        acc = __builtin_fmaf(cv[s], hs[s], acc);
     }
     if (LANES == 4) {
         acc += __shfl_xor(acc, 1, 4);
@@ -47,8 +64,8 @@ __global__ __launch_bounds__(256) void scan_step_kernel(StepParams p) {
 #pragma unroll
     for (int s = 0; s < S; ++s) p.h[r * N + part * S + s] = hs[s];
     if (part == 0) {
-        float yv = __builtin_fmaf(p.Dskip ? p.Dskip[d] : 0.0f, x, acc);
-        if (p.z) yv *= silu_f32(Act<IN>::ld(p.z, r));
+        float yv = __builtin_fmaf(dskip, x, acc);
+        if (p.z) yv *= silu_f32(z_raw);
         st_out<OUT>(p.y, r, yv);
     }
 }
