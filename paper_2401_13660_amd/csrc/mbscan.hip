@@ -68,7 +68,9 @@ bool tiled_ok(const ScanParams &p, int64_t N, int32_t in_dtype, int32_t out_dtyp
     for (const void *q : ptrs)
         if (q && !aligned(q, 16)) return false;
     (void)in_dtype; (void)out_dtype;
-    return p.batch * ((p.dim + 7) / 8) < (int64_t(1) << 33);
+    // fewer than 2^30 eight-channel waves: the kernel indexes its waves in 32 bits
+    // (with time segments, only shapes of a few thousand waves are multiplied)
+    return p.batch * ((p.dim + 7) / 8) < (int64_t(1) << 30);
 }
 
 template <int IN, int OUT>

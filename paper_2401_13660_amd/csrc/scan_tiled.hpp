@@ -138,19 +138,22 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     const int lane = threadIdx.x & 63;
     const int j = lane >> 3;          // channel within the wave
     const int q = lane & 7;           // state pair; also the timestep quad of phases A and C
-    const int64_t n_cg = (p.dim + kCh - 1) / kCh;
-    const int64_t nseg = (p.seqlen + seg_len - 1) / seg_len;
+    // Wave indexing in 32 bits: the host launches fewer than 2^31 waves and
+    // sends sequences shorter than 2^25 bytes here, so every quotient below fits.
+    const uint32_t n_cg = (uint32_t)((p.dim + kCh - 1) / kCh);
+    const uint32_t nseg = ((uint32_t)p.seqlen + (uint32_t)seg_len - 1) / (uint32_t)seg_len;
     // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2);
     // renumber them so that an XCD works on a contiguous range of (batch,
     // channel) groups and the B/C rows of a batch stay in one or two L2s.
-    const int64_t per_xcd = (int64_t)gridDim.x / 8;
-    const int64_t blk = blockIdx.x;
-    const int64_t lwg = blk < per_xcd * 8 ? (blk % 8) * per_xcd + blk / 8 : blk;
-    const int64_t wid = lwg * kWavesPerGroup + wave;
-    if (wid >= n_cg * p.batch * (PREPASS ? nseg - 1 : nseg)) return;   // whole wave leaves together
-    const int64_t cg = wid % n_cg;
-    const int64_t b = (wid / n_cg) % p.batch;
-    const int64_t seg = wid / (n_cg * p.batch);
+    const uint32_t per_xcd = gridDim.x / 8;
+    const uint32_t blk = blockIdx.x;
+    const uint32_t lwg = blk < per_xcd * 8 ? (blk % 8) * per_xcd + blk / 8 : blk;
+    const uint32_t wid = lwg * kWavesPerGroup + wave;
+    if (wid >= n_cg * (uint32_t)p.batch * (PREPASS ? nseg - 1 : nseg)) return;   // whole wave leaves together
+    const uint32_t cgb = wid / n_cg;
+    const int64_t cg = wid - cgb * n_cg;
+    const int64_t seg = cgb / (uint32_t)p.batch;
+    const int64_t b = cgb - (uint32_t)seg * (uint32_t)p.batch;
     const int64_t t_begin = seg * seg_len;
     const int64_t t_end = t_begin + seg_len < p.seqlen ? t_begin + seg_len : p.seqlen;
 
@@ -338,7 +341,8 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         wave_sync();
 
         // refill this slot with the chunk after next while the recurrence runs
-        issue_loads(sl, (uint32_t)(t0 - t_begin) + 2 * kT);
+        // (a 16-byte sequence has no next chunk)
+        if constexpr (!SHORT) issue_loads(sl, (uint32_t)(t0 - t_begin) + 2 * kT);
 
         // ---- B: the recurrence, fully unrolled over the chunk; the operands of
         //      step i + 1 are read from LDS while step i computes ----------------
@@ -436,14 +440,18 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     };
 
     issue_loads(s0, 0);
-    issue_loads(s1, kT);
-    int64_t t0 = t_begin;
-    for (; t0 + 2 * kT <= t_end; t0 += 2 * kT) {   // pairs of full chunks
-        chunk(s0, t0);
-        chunk(s1, t0 + kT);
+    if constexpr (SHORT) {
+        chunk(s0, t_begin);                         // the one half chunk
+    } else {
+        issue_loads(s1, kT);
+        int64_t t0 = t_begin;
+        for (; t0 + 2 * kT <= t_end; t0 += 2 * kT) {   // pairs of full chunks
+            chunk(s0, t0);
+            chunk(s1, t0 + kT);
+        }
+        if (t0 < t_end) chunk(s0, t0);                  // a full chunk and/or a half chunk remain
+        if (t0 + kT < t_end) chunk(s1, t0 + kT);
     }
-    if (t0 < t_end) chunk(s0, t0);                  // a full chunk and/or a half chunk remain
-    if (t0 + kT < t_end) chunk(s1, t0 + kT);
 
     if constexpr (PREPASS) {
         // the eight lanes of channel j hold its timesteps 4q .. 4q+3 of every
