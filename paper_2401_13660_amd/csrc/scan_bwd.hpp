@@ -564,16 +564,8 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
                 const f32x4 bv = bvs[k];               // (B0, B1, C0, C1)
                 const float lam0 = __builtin_fmaf(dv.z, bv.z, carry[0]);
                 const float lam1 = __builtin_fmaf(dv.z, bv.w, carry[1]);
-                const float sb = half_swap_sum(lam0 * dv.y, lam1 * dv.y);                  // dB: b5 picks the state
-                const float sc = half_swap_sum(dv.z * hb[t + 1][0], dv.z * hb[t + 1][1]);  // dC
-                const float tot = add_xor8(row_swap_sum(sb, sc));                          // b4 picks dB or dC
-                if (k & 1) {
-                    tot_hi = tot;
-                } else {                                // steps k, k + 1: b3 = 0 stores k, b3 = 1 stores k + 1
-                    const float v = b3 ? tot_hi : tot;
-                    if (WG) wg_sums[((buf * kWaves + wave) * 2 + (k >> 1)) * 64 + lane] = v;
-                    else pbc[pl + (4 * tq + k) * (kQ * 4)] = v;
-                }
+                const float pb0 = lam0 * dv.y, pb1 = lam1 * dv.y;                          // dB terms
+                const float pc0 = dv.z * hb[t + 1][0], pc1 = dv.z * hb[t + 1][1];          // dC terms
                 const float u0 = __builtin_fmaf(lam1, bv.y, lam0 * bv.x);
                 const float w0 = lam0 * ab[t][0] * hb[t][0];
                 const float w1 = lam1 * ab[t][1] * hb[t][1];
@@ -583,6 +575,18 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
                 dA[1] = __builtin_fmaf(dv.x, w1, dA[1]);
                 carry[0] = lam0 * ab[t][0];
                 carry[1] = lam1 * ab[t][1];
+                // the channel sums after the step's other work, so the swaps do not
+                // wait on the products just formed
+                const float sb = half_swap_sum(pb0, pb1);                                   // dB: b5 picks the state
+                const float sc = half_swap_sum(pc0, pc1);                                   // dC
+                const float tot = add_xor8(row_swap_sum(sb, sc));                          // b4 picks dB or dC
+                if (k & 1) {
+                    tot_hi = tot;
+                } else {                                // steps k, k + 1: b3 = 0 stores k, b3 = 1 stores k + 1
+                    const float v = b3 ? tot_hi : tot;
+                    if (WG) wg_sums[((buf * kWaves + wave) * 2 + (k >> 1)) * 64 + lane] = v;
+                    else pbc[pl + (4 * tq + k) * (kQ * 4)] = v;
+                }
             }
             sm.pa[4 * j + tq][q] = f32x4{pu[0], pu[1], pu[2], pu[3]};
             sm.pb[4 * j + tq][q] = f32x4{pd[0], pd[1], pd[2], pd[3]};

@@ -224,3 +224,28 @@ def test_step_against_oracle(N, dtype):
                                         dt_bias=inp.dt_bias, dtype=inp.dtype)
     assert rel_err(y.cpu().numpy(), yr) <= 2e-3
     assert rel_err(state.cpu().numpy(), hr) <= 1e-4
+
+
+@pytest.mark.parametrize("N", [1, 16])
+@pytest.mark.parametrize("softplus", [True, False])
+def test_step_without_optional_inputs(N, softplus):
+    """A step with no gate, no skip term and no timestep bias: the kernel reads
+    same-sized stand-ins for the absent inputs and must discard their values."""
+    import oracle
+    import paper_2401_13660_amd as mb
+    from parity import rel_err
+    inp = make_inputs(2, 45, 1, N, dtype="bf16", seed=15, with_h0=True)
+    announce(f"step without z, Dskip, dt_bias: N={N} softplus={softplus}")
+    t = to_device(inp)
+    delta = t["delta"][..., 0].contiguous()
+    if not softplus:                       # dlt = delta as given: keep it small and positive
+        delta = (delta.float().abs() * 0.05).to(delta.dtype)
+    state = t["h0"].clone()
+    y = mb.scan_step(state, t["u"][..., 0].contiguous(), delta, t["A"], t["B"][..., 0].contiguous(),
+                     t["C"][..., 0].contiguous(), delta_softplus=softplus)
+    torch.cuda.synchronize()
+    delta_bits = delta.cpu().view(torch.int16).numpy().view(np.uint16)      # the bf16 bits the GPU read
+    yr, hr = oracle.default().scan_step(inp.h0, inp.u[..., 0], delta_bits, inp.A,
+                                        inp.B[..., 0], inp.C[..., 0], delta_softplus=softplus, dtype=inp.dtype)
+    assert rel_err(y.cpu().numpy(), yr) <= 2e-3
+    assert rel_err(state.cpu().numpy(), hr) <= 1e-4
