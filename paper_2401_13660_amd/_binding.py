@@ -8,6 +8,7 @@ built library every call raises ``MBScanError``.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 
@@ -90,7 +91,31 @@ def _ptr(t):
     return None if t is None else t.data_ptr()
 
 
+# Per-call host work bounds a decode step called from Python (the kernel of a
+# one-byte step takes a few microseconds), so the stream and device lookups use
+# torch's raw accessors where it has them, and a well-formed argument passes its
+# checks in one expression.
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+_cur_device = getattr(torch._C, "_cuda_getDevice", None)
+
+
+def _stream(dev):
+    """The raw HIP stream torch currently uses on device ``dev``."""
+    if _raw_stream is not None and dev.index is not None:
+        return _raw_stream(dev.index)
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+def _on_device(dev):
+    """A context making ``dev`` current for the call; nothing if it already is."""
+    cur = _cur_device() if _cur_device is not None else torch.cuda.current_device()
+    return contextlib.nullcontext() if dev.index == cur else torch.cuda.device(dev)
+
+
 def _need(t, name, shape, dtype=None, device=None):
+    if (isinstance(t, torch.Tensor) and t.is_cuda and t.shape == shape and (dtype is None or t.dtype == dtype)
+            and (device is None or t.device == device) and t.is_contiguous()):
+        return
     if not isinstance(t, torch.Tensor):
         raise MBScanError(f"{name} must be a torch.Tensor")
     if not t.is_cuda:
@@ -172,8 +197,8 @@ def scan_fwd(u, delta, A, B, C, D=None, dt_bias=None, z=None, h0=None, *, delta_
         else:
             _need(ck, "ck", (L // 16, nb, dim, N), torch.float32, dev)
     desc = ScanDesc(nb, dim, L, N, _dt(act), _dt(out.dtype), 1 if delta_softplus else 0, 0)
-    stream = torch.cuda.current_stream(dev).cuda_stream
-    with torch.cuda.device(dev):
+    stream = _stream(dev)
+    with _on_device(dev):
         if want_ck:
             st = lib.mb_scan_fwd_ckpt(ctypes.byref(desc), _ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C),
                                       _ptr(D), _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(out), _ptr(h_last),
@@ -221,8 +246,8 @@ def scan_step(h, u_t, delta_t, A, B_t, C_t, D=None, dt_bias=None, z_t=None, *, d
         out = torch.empty((nb, dim), dtype=out_dtype, device=dev)
     else:
         _need(out, "out", (nb, dim), None, dev)
-    stream = torch.cuda.current_stream(dev).cuda_stream
-    with torch.cuda.device(dev):
+    stream = _stream(dev)
+    with _on_device(dev):
         st = lib.mb_scan_step(nb, dim, N, _dt(act), _dt(out.dtype), 1 if delta_softplus else 0,
                               _ptr(u_t), _ptr(delta_t), _ptr(A), _ptr(B_t), _ptr(C_t), _ptr(D),
                               _ptr(dt_bias), _ptr(z_t), _ptr(h), _ptr(out), stream)
@@ -260,8 +285,8 @@ def conv1d(x, w, bias=None, state=None, *, apply_silu=True, out_dtype=None, retu
     elif state_out is not None:
         _need(state_out, "state_out", (nb, dim, K - 1), torch.float32, dev)
     desc = ConvDesc(nb, dim, L, K, _dt(x.dtype), _dt(out.dtype), 1 if apply_silu else 0, 0, 0)
-    stream = torch.cuda.current_stream(dev).cuda_stream
-    with torch.cuda.device(dev):
+    stream = _stream(dev)
+    with _on_device(dev):
         st = lib.mb_conv1d_fwd(ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(bias), _ptr(state), _ptr(out),
                                _ptr(state_out) if K > 1 else None, stream)
     _check(st, "mb_conv1d_fwd")
@@ -289,8 +314,8 @@ def conv1d_step(state, x_t, w, bias=None, *, apply_silu=True, out_dtype=None, ou
         out = torch.empty((nb, dim), dtype=out_dtype or x_t.dtype, device=dev)
     else:
         _need(out, "out", (nb, dim), None, dev)
-    stream = torch.cuda.current_stream(dev).cuda_stream
-    with torch.cuda.device(dev):
+    stream = _stream(dev)
+    with _on_device(dev):
         st = lib.mb_conv1d_step(nb, dim, K, _dt(x_t.dtype), _dt(out.dtype), 1 if apply_silu else 0,
                                 _ptr(x_t), _ptr(w), _ptr(bias), _ptr(state) if K > 1 else None,
                                 _ptr(out), stream)
@@ -312,8 +337,8 @@ def verify_rank(logits, draft, beta, *, return_ranks=False):
     accepted = torch.empty(nb, dtype=torch.int32, device=dev)
     last_pos = torch.empty(nb, dtype=torch.int32, device=dev)
     ranks = torch.empty((nb, n), dtype=torch.int32, device=dev) if return_ranks else None
-    stream = torch.cuda.current_stream(dev).cuda_stream
-    with torch.cuda.device(dev):
+    stream = _stream(dev)
+    with _on_device(dev):
         st = lib.mb_verify_rank(nb, n, V, _dt(logits.dtype), int(beta), _ptr(logits), _ptr(draft),
                                 _ptr(ranks), _ptr(accepted), _ptr(last_pos), stream)
     _check(st, "mb_verify_rank")
@@ -361,8 +386,8 @@ def scan_bwd(u, delta, A, B, C, dy, D=None, dt_bias=None, z=None, h0=None, dh_la
          "ddt_bias": torch.empty(dim, **f32) if dt_bias is not None else None,
          "dh0": torch.empty((nb, dim, N), **f32)}
     desc = ScanDesc(nb, dim, L, N, _dt(act), _dt(dy.dtype), 1 if delta_softplus else 0, 0)
-    stream = torch.cuda.current_stream(dev).cuda_stream
-    with torch.cuda.device(dev):
+    stream = _stream(dev)
+    with _on_device(dev):
         st = lib.mb_scan_bwd(ctypes.byref(desc), _ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C), _ptr(D),
                              _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(dy), _ptr(dh_last), _ptr(ck),
                              _ptr(g["du"]),
