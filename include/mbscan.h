@@ -36,7 +36,10 @@
  * - Sizes: batch, dim, seqlen >= 0 (an empty problem is valid and enqueues
  *   nothing, except that seqlen == 0 still writes h_last = h0, or zeros);
  *   dstate must be 16 (the n_state of every MambaByte model, Table 9), 8, 4,
- *   2 or 1; batch * dim * seqlen must stay below 2^62.
+ *   2 or 1.  Every element count an entry point derives from its sizes
+ *   (batch * dim * seqlen, batch * dstate * seqlen, batch * dim * dstate and,
+ *   with recorded positions, npos * batch * dim * dstate) must stay below
+ *   2^56; a larger one returns MB_ERR_SHAPE.
  */
 #ifndef MBSCAN_H
 #define MBSCAN_H

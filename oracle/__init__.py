@@ -75,6 +75,8 @@ class Oracle:
         self.lib.mbo_conv1d_step.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
                                              _D, _D, _D, _D, _D]
         self.lib.mbo_max_threads.restype = ctypes.c_int
+        self.lib.mbo_set_threads.restype = None
+        self.lib.mbo_set_threads.argtypes = [ctypes.c_int]
         self.lib.mbo_scan_step.restype = ctypes.c_int
         self.lib.mbo_scan_step.argtypes = [
             ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
@@ -82,6 +84,10 @@ class Oracle:
 
     def max_threads(self) -> int:
         return int(self.lib.mbo_max_threads())
+
+    def set_threads(self, n: int) -> None:
+        """Threads of later calls (for timing the oracle on fewer cores)."""
+        self.lib.mbo_set_threads(int(n))
 
     # -- rows ---------------------------------------------------------------
     def scan_rows(self, u, delta, A, Bm, Cm, bidx, *, z=None, Dskip=None, dt_bias=None,

@@ -463,3 +463,13 @@ int mbo_max_threads(void)
     return 1;
 #endif
 }
+
+/* Set the number of threads later row loops use (the single-threaded timing). */
+void mbo_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}

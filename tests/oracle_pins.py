@@ -13,6 +13,7 @@ from __future__ import annotations
 
 import json
 import os
+import sys
 from decimal import Decimal
 
 import numpy as np
@@ -334,6 +335,78 @@ def pin_states_at_positions(orc):
                 _close(hp[k, b], ref, 1e-11, f"state at position {p} (seed {seed}, k {k}, b {b})")
 
 
+def _module_of(orc):
+    """The module that defines the oracle under test (a mutated copy in the mutant tests)."""
+    return sys.modules[type(orc).__module__]
+
+
+def pin_bf16_decode(orc):
+    """BF16 mixed precision (Section 4): the oracle reads a bf16 activation as the exact
+    value its bit pattern encodes.  All 65,536 patterns are decoded and compared with
+    torch's own bfloat16 -> float conversion (an independent library routine) and with
+    hand-worked values; then a scan and a step given bit patterns must equal the same
+    scan and step given the decoded values as floats."""
+    import torch
+    m = _module_of(orc)
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    with np.errstate(invalid="ignore"):                # signalling-NaN patterns
+        got = m.to_f64(bits, "bf16")
+    ref = torch.from_numpy(bits.view(np.int16).copy()).view(torch.bfloat16).to(torch.float64).numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan), "bf16 NaN patterns decoded wrongly"
+    assert np.array_equal(got[~nan], ref[~nan]), "bf16 decode differs from torch's conversion"
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan])), "bf16 sign decoded wrongly"
+    # sign | 8-bit exponent (bias 127) | 7-bit fraction
+    hand = {0x3F80: 1.0, 0xBF80: -1.0, 0x4000: 2.0, 0xC0A0: -5.0, 0x3FC0: 1.5, 0x4049: 3.140625,
+            0x3C00: 2.0 ** -7, 0x0080: 2.0 ** -126, 0x0001: 2.0 ** -133, 0x8000: -0.0,
+            0x7F80: np.inf, 0xFF80: -np.inf, 0x7F7F: (2.0 - 2.0 ** -7) * 2.0 ** 127}
+    for b, v in hand.items():
+        g = m.to_f64(np.array([b], np.uint16), "bf16")[0]
+        assert g == v and np.signbit(g) == np.signbit(v), f"bf16 {b:#06x} -> {g!r}, expected {v!r}"
+    # the same decode inside the scan and the step
+    c = _rand_case(31, nb=2, dim=3, L=24, N=4)
+    keys = ("u", "delta", "z", "B", "C")
+    bf = {k: torch.from_numpy(np.asarray(c[k], np.float32)).to(torch.bfloat16) for k in keys}
+    as_bits = {k: v.view(torch.int16).numpy().view(np.uint16) for k, v in bf.items()}
+    as_vals = {k: v.to(torch.float64).numpy() for k, v in bf.items()}
+    common = dict(Dskip=c["Dskip"], dt_bias=c["dt_bias"], h0=c["h0"])
+    y1, h1 = orc.scan_fwd(as_bits["u"], as_bits["delta"], c["A"], as_bits["B"], as_bits["C"],
+                          z=as_bits["z"], dtype="bf16", **common)
+    y2, h2 = orc.scan_fwd(as_vals["u"], as_vals["delta"], c["A"], as_vals["B"], as_vals["C"],
+                          z=as_vals["z"], **common)
+    assert np.array_equal(y1, y2) and np.array_equal(h1, h2), "bf16 scan differs from the decoded scan"
+    t = 5
+    s1 = orc.scan_step(c["h0"], as_bits["u"][..., t], as_bits["delta"][..., t], c["A"],
+                       as_bits["B"][..., t], as_bits["C"][..., t], z_t=as_bits["z"][..., t],
+                       Dskip=c["Dskip"], dt_bias=c["dt_bias"], dtype="bf16")
+    s2 = orc.scan_step(c["h0"], as_vals["u"][..., t], as_vals["delta"][..., t], c["A"],
+                       as_vals["B"][..., t], as_vals["C"][..., t], z_t=as_vals["z"][..., t],
+                       Dskip=c["Dskip"], dt_bias=c["dt_bias"])
+    assert np.array_equal(s1[0], s2[0]) and np.array_equal(s1[1], s2[1]), "bf16 step differs"
+
+
+def pin_rows_selection(orc):
+    """``rows=`` (how the full-size workloads are sampled) returns exactly the flat rows
+    b * dim + d it names, in the order given: unsorted rows spread over three batch
+    elements equal the time-grid closed form of those (b, d), and so do their states
+    at requested positions."""
+    c = _rand_case(33, nb=3, dim=5, L=20, N=3)
+    nb, dim, L = c["u"].shape
+    rows = np.array([14, 0, 7, 5, 9, 3, 12, 13])
+    pos = np.array([[4, -1, L - 1], [L - 1, 7, 0]])       # (npos, batch)
+    y, h, hp = _run(orc, c, rows=rows, positions=pos)
+    ry, rh, rall = _brute(c, all_states=True)
+    _close(y, ry.reshape(nb * dim, L)[rows], 1e-11, "rows= y")
+    _close(h, rh.reshape(nb * dim, -1)[rows], 1e-11, "rows= h_last")
+    assert hp.shape == (pos.shape[0], rows.size, c["A"].shape[1])
+    for i, r in enumerate(rows):
+        b, d = divmod(int(r), dim)
+        for k in range(pos.shape[0]):
+            p = pos[k, b]
+            ref = c["h0"][b, d] if p == -1 else rall[b, d, p]
+            _close(hp[k, i], ref, 1e-11, f"rows= state at position {p} of row {r}")
+
+
 # ---- the backward of the scan: reverse-mode gradients against central finite
 #      differences of the (pinned) forward -----------------------------------
 
@@ -498,7 +571,7 @@ def pin_conv_split_and_step(orc):
 ALL_PINS = [
     pin_golden_decimal, pin_bruteforce, pin_geometric, pin_B_zero, pin_split, pin_eq4,
     pin_tuple_scan, pin_separability, pin_linearity, pin_step_equals_fwd, pin_limits,
-    pin_softplus_extremes, pin_states_at_positions,
+    pin_softplus_extremes, pin_states_at_positions, pin_bf16_decode, pin_rows_selection,
     pin_conv_library, pin_conv_impulse, pin_conv_split_and_step,
     pin_bwd_finite_differences, pin_bwd_geometric, pin_bwd_linearity,
 ]

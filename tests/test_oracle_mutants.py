@@ -76,15 +76,38 @@ MUTANTS = [
 ]
 
 
-def _run_pins(lib_path):
-    orc = oracle.Oracle(lib_path)
+# Mistakes in the Python side of the oracle (oracle/__init__.py): the bf16 decode
+# every bf16 input goes through, and the row selection that samples the full-size
+# workloads.  Several leave the whole-tensor path unchanged, so only the pins of
+# those two helpers can catch them.
+PY_SRC = os.path.join(os.path.dirname(oracle.__file__), "__init__.py")
+PY_MUTANTS = [
+    ("bf16_shift_15", "astype(np.uint32) << 16", "astype(np.uint32) << 15"),
+    ("bf16_not_shifted", "astype(np.uint32) << 16", "astype(np.uint32)"),
+    ("bf16_value_cast", "bits.view(np.float32)", "bits.astype(np.float32)"),
+    ("bf16_sign_dropped", "np.ascontiguousarray(x, dtype=np.uint16).astype(np.uint32) << 16",
+     "(np.ascontiguousarray(x, dtype=np.uint16).astype(np.uint32) & 0x7FFF) << 16"),
+    ("bf16_rounded_to_f32_then_bf16", "return bits.view(np.float32).astype(np.float64)",
+     "return (bits & 0xFFFE0000).view(np.float32).astype(np.float64)"),
+    ("rows_batch_mod", "bidx = flat // dim", "bidx = flat % nb"),
+    ("rows_sorted", "reshape(nb * dim, -1)[flat]", "reshape(nb * dim, -1)[np.sort(flat)]"),
+    ("rows_h0_prefix", "reshape(nb * dim, N)[flat]", "reshape(nb * dim, N)[:len(flat)]"),
+    ("rows_A_by_position", "Af = to_f64(A)[didx]", "Af = to_f64(A)[np.arange(len(flat)) % A.shape[0]]"),
+    ("rows_skip_by_position", "to_f64(Dskip)[didx]", "to_f64(Dskip)[np.arange(len(flat)) % dim]"),
+    ("rows_positions_first_batch", "row_pos = np.ascontiguousarray(pos[:, bidx].T)",
+     "row_pos = np.ascontiguousarray(pos[:, np.sort(bidx)].T)"),
+]
+
+
+def _run_pins(lib_path, module=oracle):
+    orc = module.Oracle(lib_path)
     failed = []
     for pin in P.ALL_PINS:
         try:
             pin(orc)
         except AssertionError as e:
             failed.append(f"{pin.__name__}: {e}")
-        except (ValueError, FloatingPointError, OverflowError) as e:
+        except (ValueError, FloatingPointError, OverflowError, IndexError, TypeError) as e:
             failed.append(f"{pin.__name__}: raised {type(e).__name__}")
     return failed
 
@@ -101,3 +124,39 @@ def test_pins_catch_mutant(tmp_path, name, old, new):
     oracle.build(src=str(path), out=lib)
     failed = _run_pins(lib)
     assert failed, f"no pin caught the planted mistake {name!r}"
+
+
+@pytest.mark.parametrize("name,old,new", PY_MUTANTS, ids=[m[0] for m in PY_MUTANTS])
+def test_pins_catch_python_mutant(tmp_path, name, old, new):
+    import importlib.util
+    import sys
+    src = open(PY_SRC).read()
+    assert src.count(old) >= 1, f"mutation target for {name} not found: the oracle changed"
+    path = tmp_path / f"oracle_mut_{name}.py"
+    path.write_text(src.replace(old, new, 1))
+    modname = f"oracle_mut_{name}"
+    spec = importlib.util.spec_from_file_location(modname, path)
+    mod = importlib.util.module_from_spec(spec)
+    sys.modules[modname] = mod
+    try:
+        spec.loader.exec_module(mod)
+        failed = _run_pins(oracle.LIB_PATH, mod)
+    finally:
+        del sys.modules[modname]
+    assert failed, f"no pin caught the planted mistake {name!r}"
+
+
+def test_unmutated_python_oracle_passes(tmp_path):
+    """The mechanism above, with no mutation, leaves every pin green."""
+    import importlib.util
+    import sys
+    path = tmp_path / "oracle_copy.py"
+    path.write_text(open(PY_SRC).read())
+    spec = importlib.util.spec_from_file_location("oracle_copy", path)
+    mod = importlib.util.module_from_spec(spec)
+    sys.modules["oracle_copy"] = mod
+    try:
+        spec.loader.exec_module(mod)
+        assert _run_pins(oracle.LIB_PATH, mod) == []
+    finally:
+        del sys.modules["oracle_copy"]
