@@ -19,9 +19,12 @@ __device__ __forceinline__ float bf16_lo(uint32_t pair) { return __uint_as_float
 __device__ __forceinline__ float bf16_hi(uint32_t pair) { return __uint_as_float(pair & 0xffff0000u); }
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
-// Round to nearest even (NaN inputs are not expected on this path).
+// Round to nearest even.  A NaN stays a NaN (quiet, sign kept): adding the
+// rounding bias to a NaN with its high mantissa bits set would carry into the
+// exponent and sign and turn it into a zero.
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
     uint32_t x = __float_as_uint(f);
+    if ((x & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((x >> 16) | 0x40u);
     x += 0x7fffu + ((x >> 16) & 1u);
     return (uint16_t)(x >> 16);
 }

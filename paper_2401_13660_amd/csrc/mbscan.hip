@@ -602,7 +602,9 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     // timestep as the pass itself, so it takes the segments only with at most a
     // third as many waves as the chip holds.
     const int64_t ck_nseg = (!ck && 3 * ((D + W::kCh - 1) / W::kCh * B) <= mbs::tiled::resident_waves()) ? nseg : 1;
-    const size_t fagg_b = ck_nseg > 1 ? (size_t)(ck_nseg - 1) * (size_t)rows * W::kN * 2 * 4 : 0;
+    // the forward pre-pass writes ck_nseg planes: the aggregates of segments
+    // 0 .. ck_nseg-2 and a copy of h0 (which scan_ckpt does not need)
+    const size_t fagg_b = ck_nseg > 1 ? (size_t)ck_nseg * (size_t)rows * W::kN * 2 * 4 : 0;
     char *ws = nullptr;
     e = hipMallocAsync(reinterpret_cast<void **>(&ws), ck_b + bcp_b + row_b + agg_b + fagg_b, st);
     if (e != hipSuccess) return MB_ERR_HIP;

@@ -120,6 +120,11 @@ struct WaveSmemPre {
 //   end state H[n]; written to carry[((seg * rows + row) * 16 + n) * 2 + {0, 1}].
 //   Folding h <- P h + H is the associative operator of the parallel-scan
 //   formulation (Section 2, "Implementation") applied across segments.
+//   The waves of segment 0 also copy h0 (or zeros) into plane nseg - 1 as the
+//   pairs (1, h0[n]).  With several segments the scan starts every segment from
+//   zero and folds that plane first, so it never reads h0 itself: the wave of
+//   the last segment may then write h_last over h0 while the waves of earlier
+//   segments of the same rows have not started (workgroups are not ordered).
 // POS = true (scan only): also record the states at p.pos (p.npos > 0).
 // CK = true (scan only): also store the state at every 16-timestep boundary in
 //   p.ck, the checkpoints the backward recomputes its chunks from.
@@ -169,15 +174,24 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
         a2[s] = p.A[dcl * kN + n0 + s] * kLog2e;
-        h[s] = (!PREPASS && p.h0) ? p.h0[row * kN + n0 + s] : 0.0f;
+        h[s] = (!PREPASS && nseg == 1 && p.h0) ? p.h0[row * kN + n0 + s] : 0.0f;
     }
-    if (!PREPASS) {
-        // carry-in: fold the aggregates of the earlier segments into h0
-        for (int64_t s2 = 0; s2 < seg; ++s2) {
-            const f32x4 ph = *reinterpret_cast<const f32x4 *>(carry + ((s2 * rows + row) * kN + n0) * 2);
+    if (!PREPASS && nseg > 1) {
+        // carry-in: the copy of h0 (plane nseg - 1), then the aggregates of the
+        // earlier segments; folding (1, h0) into the zero state gives h0 exactly
+        auto fold = [&](int64_t plane) {
+            const f32x4 ph = *reinterpret_cast<const f32x4 *>(carry + ((plane * rows + row) * kN + n0) * 2);
             h[0] = __builtin_fmaf(ph.x, h[0], ph.y);
             h[1] = __builtin_fmaf(ph.z, h[1], ph.w);
-        }
+        };
+        fold(nseg - 1);
+        for (int64_t s2 = 0; s2 < seg; ++s2) fold(s2);
+    }
+    if (PREPASS && seg == 0 && live) {
+        const float g0 = p.h0 ? p.h0[row * kN + n0] : 0.0f;
+        const float g1 = p.h0 ? p.h0[row * kN + n0 + 1] : 0.0f;
+        *reinterpret_cast<f32x4 *>(carry + (((int64_t)(nseg - 1) * rows + row) * kN + n0) * 2) =
+            f32x4{1.0f, g0, 1.0f, g1};
     }
     float dsum = 0.0f;      // PREPASS: this lane's share of the segment's sum of dlt
     const float dskip = p.Dskip ? p.Dskip[dcl] : 0.0f;
@@ -513,7 +527,8 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
     const size_t lds = sizeof(WaveSmem) * kWavesPerGroup;
     hipError_t e;
     if (nseg > 1) {
-        const size_t bytes = (size_t)(nseg - 1) * (size_t)(p.batch * p.dim) * kN * 2 * sizeof(float);
+        // the aggregates of segments 0 .. nseg-2, then the copy of h0
+        const size_t bytes = (size_t)nseg * (size_t)(p.batch * p.dim) * kN * 2 * sizeof(float);
         e = hipMallocAsync(reinterpret_cast<void **>(&carry), bytes, st);
         if (e != hipSuccess) return e;
         const int64_t waves = n_cg * p.batch * (nseg - 1);
