@@ -13,6 +13,7 @@
 #include "scan_rowwise.hpp"
 #include "scan_step.hpp"
 #include "scan_tiled.hpp"
+#include "scan_ts2.hpp"
 #include "verify_rank.hpp"
 
 namespace {
@@ -75,9 +76,12 @@ bool tiled_ok(const ScanParams &p, int64_t N, int32_t in_dtype, int32_t out_dtyp
 
 template <int IN, int OUT>
 hipError_t fwd_dispatch_n(ScanParams &p, int64_t N, void *stream) {
-    if (tiled_ok(p, N, IN, OUT))
+    if (tiled_ok(p, N, IN, OUT)) {
+        if (mbs::ts2::takes(p))
+            return p.z ? mbs::ts2::fwd_ts2<IN, OUT, true>(p, stream) : mbs::ts2::fwd_ts2<IN, OUT, false>(p, stream);
         return p.z ? mbs::tiled::fwd_tiled<IN, OUT, true>(p, stream)
                    : mbs::tiled::fwd_tiled<IN, OUT, false>(p, stream);
+    }
     switch (N) {
         case 1: return fwd_rowwise<IN, OUT, 1>(p, stream);
         case 2: return fwd_rowwise<IN, OUT, 2>(p, stream);

@@ -131,6 +131,15 @@ struct WaveSmemPre {
 // SHORT = true (scan only, seqlen 16): one half chunk per wave, with the
 //   half-size tables of WaveSmemT<true>; phases A and C give every lane two
 //   timesteps (2q, 2q+1) instead of four to half of them.
+template <int N> __device__ __forceinline__ void lds_wait() {
+    static_assert(N >= 0 && N < 16, "lgkmcnt is a 4-bit field");
+    // nothing may be scheduled across the wait, so that the reads issued after
+    // it stay after it and the operands read before it need no further wait
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0xC07F | (N << 8));
+    __builtin_amdgcn_sched_barrier(0);
+}
+
 template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool PREPASS, bool POS, bool CK = false,
           bool SHORT = false>
 __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len, float *carry) {
@@ -273,6 +282,9 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
             for (int k = 0; k < 4; ++k) bcv[k] = sm.bc[4 * TQ + k][q];
         }
     };
+    // s_waitcnt lgkmcnt(N) (vmcnt and expcnt left alone): wait until at most N of
+    // this wave's LDS operations are outstanding.
+    constexpr int kW = PREPASS ? 0 : 1;      // the scan writes one partial row per step
     // Order this wave's LDS writes before its later reads of other lanes' data.
     auto wave_sync = [] {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -373,25 +385,38 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
             using I5 = std::integral_constant<int, 5>;
             using I6 = std::integral_constant<int, 6>;
             using I7 = std::integral_constant<int, 7>;
+            // One wait per step: before step i computes, its operands (read
+            // during step i - 1) must have arrived, while the partial row that
+            // step i - 1 wrote may still be in flight (LDS operations complete
+            // in order).  The reads of step i + 1 go out right after the wait.
             load4(ddA, bcA, I0{});
+            lds_wait<0>();
             load4(ddB, bcB, I1{});
             recur4(ddA, bcA, I0{});
+            lds_wait<kW>();
             load4(ddA, bcA, I2{});
             recur4(ddB, bcB, I1{});
+            lds_wait<kW>();
             load4(ddB, bcB, I3{});
             recur4(ddA, bcA, I2{});
             if (!SHORT && nt == kT) {
+                lds_wait<kW>();
                 load4(ddA, bcA, I4{});
                 recur4(ddB, bcB, I3{});
                 if (CK) store_ck();
+                lds_wait<kW>();
                 load4(ddB, bcB, I5{});
                 recur4(ddA, bcA, I4{});
+                lds_wait<kW>();
                 load4(ddA, bcA, I6{});
                 recur4(ddB, bcB, I5{});
+                lds_wait<kW>();
                 load4(ddB, bcB, I7{});
                 recur4(ddA, bcA, I6{});
+                lds_wait<kW>();
                 recur4(ddB, bcB, I7{});
             } else {                                // nt == 16: the last, half chunk
+                lds_wait<kW>();
                 recur4(ddB, bcB, I3{});
             }
         }
@@ -507,14 +532,30 @@ inline int64_t choose_segments(int64_t waves_base, int64_t L, int64_t resident, 
     return (L + len - 1) / len;
 }
 
-// Waves of the scan resident at once on the current device (2 workgroups of
-// 4 waves per CU); 256 CUs if the runtime cannot say.
-inline int64_t resident_waves() {
+// Compute units of the current device; 256 (MI355X) if the runtime cannot say.
+inline int64_t device_cus() {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
         cus = 256;
-    return 2 * kWavesPerGroup * (int64_t)cus;
+    return cus;
+}
+
+// Waves of the scan resident at once on the current device (2 workgroups of
+// 4 waves per CU).
+inline int64_t resident_waves() { return 2 * kWavesPerGroup * device_cus(); }
+
+// The time segments the forward takes for p (1: none), and their length.
+inline int64_t fwd_segments(const ScanParams &p, int64_t *seg_len) {
+    const int64_t n_cg = (p.dim + kCh - 1) / kCh;
+    *seg_len = p.seqlen;
+    return p.seqlen >= 512 ? choose_segments(n_cg * p.batch, p.seqlen, resident_waves(), seg_len) : 1;
+}
+
+// Device bytes of the segment carry: the aggregates of segments 0 .. nseg-2,
+// then the copy of h0 (rows x 16 states x 2 floats per plane).
+inline size_t fwd_carry_bytes(const ScanParams &p, int64_t nseg) {
+    return nseg > 1 ? (size_t)nseg * (size_t)(p.batch * p.dim) * kN * 2 * sizeof(float) : 0;
 }
 
 template <int IN, int OUT, bool GATE, bool SP>
@@ -522,14 +563,12 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
     hipStream_t st = static_cast<hipStream_t>(stream);
     const int64_t n_cg = (p.dim + kCh - 1) / kCh;
     int64_t seg_len = p.seqlen;
-    const int64_t nseg = p.seqlen >= 512 ? choose_segments(n_cg * p.batch, p.seqlen, resident_waves(), &seg_len) : 1;
+    const int64_t nseg = fwd_segments(p, &seg_len);
     float *carry = nullptr;
     const size_t lds = sizeof(WaveSmem) * kWavesPerGroup;
     hipError_t e;
     if (nseg > 1) {
-        // the aggregates of segments 0 .. nseg-2, then the copy of h0
-        const size_t bytes = (size_t)nseg * (size_t)(p.batch * p.dim) * kN * 2 * sizeof(float);
-        e = hipMallocAsync(reinterpret_cast<void **>(&carry), bytes, st);
+        e = hipMallocAsync(reinterpret_cast<void **>(&carry), fwd_carry_bytes(p, nseg), st);
         if (e != hipSuccess) return e;
         const int64_t waves = n_cg * p.batch * (nseg - 1);
         const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;

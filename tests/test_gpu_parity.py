@@ -171,6 +171,35 @@ def test_h_last_may_alias_h0_segmented(shape, entry):
         assert rel_err(hp, hp_ref) <= 1e-4
 
 
+# Shapes with at most one plain-kernel wave per SIMD and one time segment take the
+# kernel that cuts every chunk into two time slices inside the wave; the
+# checkpointing entry point always takes the plain kernel.  Both compute each
+# state by the same operations in the same order, so y and h_last must be equal
+# bit for bit (and both meet the oracle).
+@pytest.mark.parametrize("shape,dtype,out_dtype,gated,with_h0,softplus", [
+    ((4, 2048, 512), "bf16", torch.float32, True, False, True),       # 1024 plain waves
+    ((3, 100, 320), "f32", torch.bfloat16, False, True, False),       # dead lanes, half chunk
+    ((1, 8, 48), "bf16", torch.float32, True, True, True),            # one full and one half chunk
+    ((2, 36, 32), "f32", torch.float32, True, True, True),            # a single full chunk
+])
+def test_time_split_kernel_equals_plain(shape, dtype, out_dtype, gated, with_h0, softplus):
+    import paper_2401_13660_amd as mb
+    nb, dim, L = shape
+    inp = make_inputs(nb, dim, L, 16, dtype=dtype, seed=31, gated=gated, with_h0=with_h0)
+    announce(f"time-split vs plain kernel {shape} {dtype} out={out_dtype} gated={gated} h0={with_h0}")
+    t = to_device(inp)
+    kw = dict(D=t["Dskip"], dt_bias=t["dt_bias"], z=t.get("z"), h0=t.get("h0"), delta_softplus=softplus,
+              out_dtype=out_dtype)
+    y1, h1 = mb.scan_fwd(t["u"], t["delta"], t["A"], t["B"], t["C"], return_last_state=True, **kw)
+    y2, h2, _ = mb.scan_fwd(t["u"], t["delta"], t["A"], t["B"], t["C"], return_last_state=True,
+                            return_ckpt=True, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2), "y differs between the time-split and the plain kernel"
+    assert torch.equal(h1, h2), "h_last differs between the time-split and the plain kernel"
+    tol = TOL_Y_BF16_OUT if out_dtype == torch.bfloat16 else 2e-3
+    check_against_oracle(inp, y1, h1, tol_y=tol, delta_softplus=softplus)
+
+
 def test_resume_split_on_gpu():
     """Scanning two halves with the carried state equals scanning the whole (Alg. 1 resume)."""
     import paper_2401_13660_amd as mb
