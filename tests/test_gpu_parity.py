@@ -185,10 +185,16 @@ def test_h_last_may_alias_h0_segmented(shape, entry):
 def test_time_split_kernel_equals_plain(shape, dtype, out_dtype, gated, with_h0, softplus):
     import paper_2401_13660_amd as mb
     nb, dim, L = shape
-    inp = make_inputs(nb, dim, L, 16, dtype=dtype, seed=31, gated=gated, with_h0=with_h0)
-    announce(f"time-split vs plain kernel {shape} {dtype} out={out_dtype} gated={gated} h0={with_h0}")
+    inp = make_inputs(nb, dim, L, 16, dtype=dtype, seed=31, gated=gated, with_h0=with_h0,
+                      with_bias=softplus)
+    if not softplus:
+        # used as given, Delta must stay positive (else abar > 1 and the state grows without bound)
+        assert dtype == "f32"
+        inp.delta = np.abs(inp.delta).astype(np.float32) * np.float32(0.05)
+    announce(f"time-split vs plain kernel {shape} {dtype} out={out_dtype} gated={gated} h0={with_h0} "
+             f"softplus={softplus}")
     t = to_device(inp)
-    kw = dict(D=t["Dskip"], dt_bias=t["dt_bias"], z=t.get("z"), h0=t.get("h0"), delta_softplus=softplus,
+    kw = dict(D=t["Dskip"], dt_bias=t.get("dt_bias"), z=t.get("z"), h0=t.get("h0"), delta_softplus=softplus,
               out_dtype=out_dtype)
     y1, h1 = mb.scan_fwd(t["u"], t["delta"], t["A"], t["B"], t["C"], return_last_state=True, **kw)
     y2, h2, _ = mb.scan_fwd(t["u"], t["delta"], t["A"], t["B"], t["C"], return_last_state=True,
