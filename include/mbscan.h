@@ -108,6 +108,30 @@ int mb_scan_fwd(const mb_scan_desc *desc,
                 const float *h0, void *y, float *h_last, void *stream);
 
 /*
+ * mb_scan_fwd for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  The
+ * arguments, the results (the same bits as mb_scan_fwd's) and the errors are
+ * those of mb_scan_fwd; the call itself allocates nothing.
+ *
+ * Where mb_scan_fwd cuts a sequence into time segments (few rows, long
+ * sequences) it allocates a carry buffer of nseg x batch x dim x 128 bytes on
+ * the stream.  This entry point keeps that carry in a static device array of
+ * 8 MiB instead: each GPU the library runs on holds its own copy until the
+ * process ends.  A problem whose carry would exceed it returns MB_ERR_SHAPE
+ * (on a 256-CU MI355X the forward's segment choice never needs more than
+ * 4 MiB).  The array keeps the last call's contents; nothing in it needs to
+ * start at zero (the segment pre-pass writes every carry entry before the scan
+ * reads it).  Every call on one GPU shares that GPU's array, so calls that may
+ * overlap in time on one GPU (other streams, other threads) race: serialise
+ * them, or use mb_scan_fwd.
+ */
+int mb_scan_fwd_noalloc(const mb_scan_desc *desc,
+                        const void *u, const void *delta, const float *A,
+                        const void *Bmat, const void *Cmat,
+                        const float *Dskip, const float *dt_bias, const void *z,
+                        const float *h0, void *y, float *h_last, void *stream);
+
+/*
  * mb_scan_fwd that also records the state at requested positions.  The
  * verifier of Algorithm 1 (Appendix F) scans the drafted bytes in parallel,
  * finds the bifurcation position c and continues byte by byte from h_c; the

@@ -52,6 +52,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib = ctypes.CDLL(path)
     lib.mb_scan_fwd.restype = ctypes.c_int
     lib.mb_scan_fwd.argtypes = [ctypes.POINTER(ScanDesc)] + [_VP] * 12
+    lib.mb_scan_fwd_noalloc.restype = ctypes.c_int
+    lib.mb_scan_fwd_noalloc.argtypes = [ctypes.POINTER(ScanDesc)] + [_VP] * 12
     lib.mb_scan_fwd_states.restype = ctypes.c_int
     lib.mb_scan_fwd_states.argtypes = [ctypes.POINTER(ScanDesc)] + [_VP] * 11 + [_VP, ctypes.c_int64, _VP, _VP]
     lib.mb_scan_step.restype = ctypes.c_int
@@ -220,6 +222,39 @@ def scan_fwd(u, delta, A, B, C, D=None, dt_bias=None, z=None, h0=None, *, delta_
     if want_ck:
         res += (ck,)
     return res[0] if len(res) == 1 else res
+
+
+def scan_fwd_noalloc(u, delta, A, B, C, D=None, dt_bias=None, z=None, h0=None, *, out, h_last=None,
+                     delta_softplus=True):
+    """scan_fwd through mb_scan_fwd_noalloc: nothing is allocated, so the output y
+    (``out``) and, if wanted, ``h_last`` are given by the caller (h_last may be h0).
+    Returns y or (y, h_last)."""
+    lib = load_library()
+    if not isinstance(u, torch.Tensor) or u.dim() != 3 or not isinstance(A, torch.Tensor) or A.dim() != 2:
+        raise MBScanError("u must be a (batch, dim, L) tensor and A a (dim, N) tensor")
+    nb, dim, L = u.shape
+    N = A.shape[1]
+    dev, act = u.device, u.dtype
+    for t, name, shape, dt in ((u, "u", (nb, dim, L), act), (delta, "delta", (nb, dim, L), act),
+                               (A, "A", (dim, N), torch.float32), (B, "B", (nb, N, L), act),
+                               (C, "C", (nb, N, L), act)):
+        _need(t, name, shape, dt, dev)
+    for t, name, shape, dt in ((z, "z", (nb, dim, L), act), (D, "D", (dim,), torch.float32),
+                               (dt_bias, "dt_bias", (dim,), torch.float32),
+                               (h0, "h0", (nb, dim, N), torch.float32),
+                               (h_last, "h_last", (nb, dim, N), torch.float32)):
+        if t is not None:
+            _need(t, name, shape, dt, dev)
+    if not isinstance(out, torch.Tensor) or out.dtype not in (torch.float32, torch.bfloat16):
+        raise MBScanError("out must be a float32 or bfloat16 tensor")
+    _need(out, "out", (nb, dim, L), out.dtype, dev)
+    desc = ScanDesc(nb, dim, L, N, _dt(act), _dt(out.dtype), 1 if delta_softplus else 0, 0)
+    with _on_device(dev):
+        st = lib.mb_scan_fwd_noalloc(ctypes.byref(desc), _ptr(u), _ptr(delta), _ptr(A), _ptr(B), _ptr(C),
+                                     _ptr(D), _ptr(dt_bias), _ptr(z), _ptr(h0), _ptr(out), _ptr(h_last),
+                                     _stream(dev))
+    _check(st, "mb_scan_fwd_noalloc")
+    return out if h_last is None else (out, h_last)
 
 
 def scan_step(h, u_t, delta_t, A, B_t, C_t, D=None, dt_bias=None, z_t=None, *, delta_softplus=True,

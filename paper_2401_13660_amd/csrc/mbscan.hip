@@ -6,6 +6,8 @@
 
 #include <stdint.h>
 
+#include <mutex>
+
 #include "conv1d.hpp"
 #include "mbscan.h"
 #include "scan_bwd.hpp"
@@ -75,12 +77,12 @@ bool tiled_ok(const ScanParams &p, int64_t N, int32_t in_dtype, int32_t out_dtyp
 }
 
 template <int IN, int OUT>
-hipError_t fwd_dispatch_n(ScanParams &p, int64_t N, void *stream) {
+hipError_t fwd_dispatch_n(ScanParams &p, int64_t N, void *stream, float *lent) {
     if (tiled_ok(p, N, IN, OUT)) {
         if (mbs::ts2::takes(p))
             return p.z ? mbs::ts2::fwd_ts2<IN, OUT, true>(p, stream) : mbs::ts2::fwd_ts2<IN, OUT, false>(p, stream);
-        return p.z ? mbs::tiled::fwd_tiled<IN, OUT, true>(p, stream)
-                   : mbs::tiled::fwd_tiled<IN, OUT, false>(p, stream);
+        return p.z ? mbs::tiled::fwd_tiled<IN, OUT, true>(p, stream, lent)
+                   : mbs::tiled::fwd_tiled<IN, OUT, false>(p, stream, lent);
     }
     switch (N) {
         case 1: return fwd_rowwise<IN, OUT, 1>(p, stream);
@@ -302,11 +304,43 @@ const char *mb_status_string(int status) {
 
 namespace {
 
+// ---- the scratch array of mb_scan_fwd_noalloc ------------------------------
+//
+// Each GPU the library runs on holds one copy of `scratch` until the process
+// ends.  In host code the name is only a stand-in for the device symbol: the
+// device address of this GPU's copy comes from hipGetSymbolAddress, looked up
+// once per device with that device current and kept in scratch_dev[].
+constexpr size_t kScratchBytes = size_t(8) << 20;
+constexpr int kMaxDevices = 64;
+void *scratch_dev[kMaxDevices];
+std::mutex scratch_mu;
+
+}  // namespace
+
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+// The device address of the current device's scratch array.
+int scratch_for_current_device(void **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return MB_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices) return MB_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (!scratch_dev[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return MB_ERR_HIP;
+        scratch_dev[dev] = ptr;
+    }
+    *out = scratch_dev[dev];
+    return MB_OK;
+}
+
 // The forward scan behind mb_scan_fwd, mb_scan_fwd_states and mb_scan_fwd_ckpt.
 int scan_fwd_impl(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
                   const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
                   const void *z, const float *h0, void *y, float *h_last, const int32_t *pos,
-                  int64_t npos, float *h_pos, float *ck, void *stream) {
+                  int64_t npos, float *h_pos, float *ck, void *stream, bool no_alloc = false) {
     if (!desc) return MB_ERR_NULL;
     const int64_t B = desc->batch, D = desc->dim, L = desc->seqlen, N = desc->dstate;
     if (B < 0 || D < 0 || L < 0 || N < 0) return MB_ERR_SHAPE;
@@ -404,11 +438,25 @@ int scan_fwd_impl(const mb_scan_desc *desc, const void *u, const void *delta, co
         return e == hipSuccess ? MB_OK : MB_ERR_HIP;
     }
 
+    float *lent = nullptr;
+    if (no_alloc && tiled_ok(p, N, desc->in_dtype, desc->out_dtype)) {
+        // the segment carry lives in this device's copy of the static scratch array
+        int64_t seg_len;
+        const size_t need = mbs::tiled::fwd_carry_bytes(p, mbs::tiled::fwd_segments(p, &seg_len));
+        if (need > kScratchBytes) return MB_ERR_SHAPE;
+        if (need > 0) {
+            const int st = scratch_for_current_device(reinterpret_cast<void **>(&lent));
+            if (st != MB_OK) return st;
+        }
+    }
+
     hipError_t e;
     if (desc->in_dtype == MB_F32)
-        e = desc->out_dtype == MB_F32 ? fwd_dispatch_n<0, 0>(p, N, stream) : fwd_dispatch_n<0, 1>(p, N, stream);
+        e = desc->out_dtype == MB_F32 ? fwd_dispatch_n<0, 0>(p, N, stream, lent)
+                                      : fwd_dispatch_n<0, 1>(p, N, stream, lent);
     else
-        e = desc->out_dtype == MB_F32 ? fwd_dispatch_n<1, 0>(p, N, stream) : fwd_dispatch_n<1, 1>(p, N, stream);
+        e = desc->out_dtype == MB_F32 ? fwd_dispatch_n<1, 0>(p, N, stream, lent)
+                                      : fwd_dispatch_n<1, 1>(p, N, stream, lent);
     return e == hipSuccess ? MB_OK : MB_ERR_HIP;
 }
 
@@ -421,6 +469,13 @@ int mb_scan_fwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
                 const void *z, const float *h0, void *y, float *h_last, void *stream) {
     return scan_fwd_impl(desc, u, delta, A, Bmat, Cmat, Dskip, dt_bias, z, h0, y, h_last, nullptr, 0, nullptr,
                          nullptr, stream);
+}
+
+int mb_scan_fwd_noalloc(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,
+                        const void *Bmat, const void *Cmat, const float *Dskip, const float *dt_bias,
+                        const void *z, const float *h0, void *y, float *h_last, void *stream) {
+    return scan_fwd_impl(desc, u, delta, A, Bmat, Cmat, Dskip, dt_bias, z, h0, y, h_last, nullptr, 0, nullptr,
+                         nullptr, stream, true);
 }
 
 int mb_scan_fwd_states(const mb_scan_desc *desc, const void *u, const void *delta, const float *A,

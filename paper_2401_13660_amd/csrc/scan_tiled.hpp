@@ -558,8 +558,10 @@ inline size_t fwd_carry_bytes(const ScanParams &p, int64_t nseg) {
     return nseg > 1 ? (size_t)nseg * (size_t)(p.batch * p.dim) * kN * 2 * sizeof(float) : 0;
 }
 
+// lent: device memory of at least fwd_carry_bytes() for the carry, or null for
+// an allocation on the stream (hipMallocAsync, freed after the scan).
 template <int IN, int OUT, bool GATE, bool SP>
-hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
+hipError_t fwd_tiled_sp(ScanParams &p, void *stream, float *lent) {
     hipStream_t st = static_cast<hipStream_t>(stream);
     const int64_t n_cg = (p.dim + kCh - 1) / kCh;
     int64_t seg_len = p.seqlen;
@@ -568,15 +570,22 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
     const size_t lds = sizeof(WaveSmem) * kWavesPerGroup;
     hipError_t e;
     if (nseg > 1) {
-        e = hipMallocAsync(reinterpret_cast<void **>(&carry), fwd_carry_bytes(p, nseg), st);
-        if (e != hipSuccess) return e;
+        if (lent) {
+            carry = lent;
+        } else {
+            e = hipMallocAsync(reinterpret_cast<void **>(&carry), fwd_carry_bytes(p, nseg), st);
+            if (e != hipSuccess) return e;
+        }
         const int64_t waves = n_cg * p.batch * (nseg - 1);
         const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;
         void *args[] = {&p, &seg_len, &carry};
         e = hipLaunchKernel(reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, true, false>),
                             dim3((unsigned)blocks), dim3(kThreads), args,
                             sizeof(WaveSmemPre) * kWavesPerGroup, st);
-        if (e != hipSuccess) { (void)hipFreeAsync(carry, st); return e; }
+        if (e != hipSuccess) {
+            if (!lent) (void)hipFreeAsync(carry, st);
+            return e;
+        }
     }
     const int64_t waves = n_cg * p.batch * nseg;
     const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;
@@ -592,7 +601,7 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
                      : reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false>);
     const size_t main_lds = short_seq ? sizeof(WaveSmemT<true>) * kWavesPerGroup : lds;
     e = hipLaunchKernel(main_fn, dim3((unsigned)blocks), dim3(kThreads), args, main_lds, st);
-    if (carry) {
+    if (carry && !lent) {
         const hipError_t f = hipFreeAsync(carry, st);
         if (e == hipSuccess) e = f;
     }
@@ -600,9 +609,9 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream) {
 }
 
 template <int IN, int OUT, bool GATE>
-hipError_t fwd_tiled(ScanParams &p, void *stream) {
-    return p.delta_softplus ? fwd_tiled_sp<IN, OUT, GATE, true>(p, stream)
-                            : fwd_tiled_sp<IN, OUT, GATE, false>(p, stream);
+hipError_t fwd_tiled(ScanParams &p, void *stream, float *lent) {
+    return p.delta_softplus ? fwd_tiled_sp<IN, OUT, GATE, true>(p, stream, lent)
+                            : fwd_tiled_sp<IN, OUT, GATE, false>(p, stream, lent);
 }
 
 }  // namespace tiled

@@ -1,0 +1,50 @@
+"""mb_scan_fwd_noalloc through the C ABI: the same bits as mb_scan_fwd, with the
+segment carry in the library's static scratch array, on two calls in a row (the
+second smaller, so it runs over what the first left in the array)."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import announce, check_against_oracle, has_gpu, to_device
+from paper_2401_13660_amd.inputs import make_inputs
+
+pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not has_gpu(), reason="needs a GPU")]
+
+
+def _both(inp):
+    import paper_2401_13660_amd as mb
+    t = to_device(inp)
+    kw = dict(D=t["Dskip"], dt_bias=t["dt_bias"], z=t["z"], h0=t["h0"])
+    y_ref, h_ref = mb.scan_fwd(t["u"], t["delta"], t["A"], t["B"], t["C"], return_last_state=True, **kw)
+    y = torch.full_like(y_ref, float("nan"))
+    h = torch.full_like(h_ref, float("nan"))
+    out = mb.scan_fwd_noalloc(t["u"], t["delta"], t["A"], t["B"], t["C"], out=y, h_last=h, **kw)
+    torch.cuda.synchronize()
+    assert out[0].data_ptr() == y.data_ptr() and out[1].data_ptr() == h.data_ptr()
+    return y_ref, h_ref, y, h
+
+
+# (1, 64, 4096): 16 time segments, (1, 40, 1024): 4 segments, (2, 72, 208): none
+# (a ragged tail chunk and dead lanes).  Each runs after the previous one.
+@pytest.mark.parametrize("shapes", [[(1, 64, 4096), (1, 40, 1024)], [(1, 61, 4112), (2, 72, 208)]])
+def test_noalloc_equals_fwd_twice(shapes):
+    for i, (nb, dim, L) in enumerate(shapes):
+        inp = make_inputs(nb, dim, L, 16, dtype="bf16", seed=40 + i, with_h0=True)
+        announce(f"mb_scan_fwd_noalloc call {i + 1}: {(nb, dim, L)}")
+        y_ref, h_ref, y, h = _both(inp)
+        assert torch.equal(y, y_ref), f"y differs from mb_scan_fwd on {(nb, dim, L)}"
+        assert torch.equal(h, h_ref), f"h_last differs from mb_scan_fwd on {(nb, dim, L)}"
+        check_against_oracle(inp, y, h)
+
+
+def test_noalloc_h_last_on_h0():
+    import paper_2401_13660_amd as mb
+    inp = make_inputs(1, 64, 4096, 16, dtype="bf16", seed=43, with_h0=True)
+    announce("mb_scan_fwd_noalloc with h_last on top of h0 (1, 64, 4096)")
+    t = to_device(inp)
+    state = t["h0"].clone()
+    y = torch.empty(inp.u.shape, dtype=torch.float32, device="cuda")
+    mb.scan_fwd_noalloc(t["u"], t["delta"], t["A"], t["B"], t["C"], D=t["Dskip"], dt_bias=t["dt_bias"],
+                        z=t["z"], h0=state, out=y, h_last=state)
+    torch.cuda.synchronize()
+    check_against_oracle(inp, y, state)
