@@ -29,9 +29,10 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(_PKG)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
-# The files that define the tiled scan kernel and its launch configuration, and
+# The files that define the forward scan kernels (plain and time-split) and their
+# launch configuration, and
 # those of the convolution kernel (its launch lives in mbscan.hip's conv_fwd_k).
-KERNEL_SOURCES = ("scan_tiled.hpp", "device_math.hpp", "scan_params.hpp")
+KERNEL_SOURCES = ("scan_tiled.hpp", "scan_ts2.hpp", "device_math.hpp", "scan_params.hpp")
 CONV_KERNEL_SOURCES = ("conv1d.hpp", "device_math.hpp")
 
 
