@@ -229,15 +229,14 @@ hipError_t bwd_launch(mbs::bwd::BwdParams &p, bool have_ck, float *dA, float *dB
         f.batch = p.batch; f.dim = p.dim; f.seqlen = p.seqlen;
         f.u = p.u; f.delta = p.delta; f.Bm = p.Bm; f.Cm = p.Cm;
         f.A = p.A; f.dt_bias = p.dt_bias;
-        f.y = p.du;                                      // never written by the pre-pass
         f.delta_softplus = p.delta_softplus;
         int64_t seg_len = p.ck_seg_len;
         float *fagg = const_cast<float *>(p.fagg);
         void *fargs[] = {&f, &seg_len, &fagg};
         namespace T = mbs::tiled;
         const dim3 grid_pre((unsigned)((waves * (ck_nseg - 1) + T::kWavesPerGroup - 1) / T::kWavesPerGroup));
-        e = hipLaunchKernel(reinterpret_cast<const void *>(&T::scan_fwd_tiled<IN, 0, false, SP, true, false>),
-                            grid_pre, dim3(T::kThreads), fargs, sizeof(T::WaveSmemPre) * T::kWavesPerGroup, st);
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&T::scan_seg_agg<IN, SP>), grid_pre, dim3(T::kThreads),
+                            fargs, sizeof(T::WaveSmemPre) * T::kWavesPerGroup, st);
         if (e != hipSuccess) return e;
     }
     if (!have_ck) {

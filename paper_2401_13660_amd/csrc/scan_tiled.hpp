@@ -104,8 +104,9 @@ template <bool SHORT> struct WaveSmemT {
 using WaveSmem = WaveSmemT<false>;
 static_assert(sizeof(WaveSmemT<true>) * kWavesPerGroup * 5 <= 160 * 1024,
               "five workgroups of the 16-timestep tables fit the 160 KB of a CU's LDS");
-// The pre-pass needs neither C nor the output partials.  It stages B two
-// timesteps per entry, and the smaller area lets more waves share a CU:
+// The segment aggregate pass (scan_seg_agg) needs neither C nor the output
+// partials.  It stages B two timesteps per entry, and the smaller area lets more
+// waves share a CU:
 //   b2    row r = timesteps 2r, 2r+1; entry q = (B[2q], B[2q+1]) at 2r, then at 2r+1
 struct WaveSmemPre {
     static constexpr int kSteps = kT;
@@ -113,24 +114,18 @@ struct WaveSmemPre {
     f32x4 b2[kT / 2][kDdRow];                 // 2.25 KB
 };
 
-// PREPASS = false: the scan itself.  With several time segments, the wave of
-//   segment s starts from h0 folded with the aggregates of segments 0..s-1.
-// PREPASS = true: for every segment but the last, the segment's aggregate from a
-//   zero state: P[n] = prod_t abar_t[n] = 2^(A[n] log2e sum_t dlt_t) and the local
-//   end state H[n]; written to carry[((seg * rows + row) * 16 + n) * 2 + {0, 1}].
-//   Folding h <- P h + H is the associative operator of the parallel-scan
-//   formulation (Section 2, "Implementation") applied across segments.
-//   The waves of segment 0 also copy h0 (or zeros) into plane nseg - 1 as the
-//   pairs (1, h0[n]).  With several segments the scan starts every segment from
-//   zero and folds that plane first, so it never reads h0 itself: the wave of
-//   the last segment may then write h_last over h0 while the waves of earlier
-//   segments of the same rows have not started (workgroups are not ordered).
-// POS = true (scan only): also record the states at p.pos (p.npos > 0).
-// CK = true (scan only): also store the state at every 16-timestep boundary in
-//   p.ck, the checkpoints the backward recomputes its chunks from.
-// SHORT = true (scan only, seqlen 16): one half chunk per wave, with the
-//   half-size tables of WaveSmemT<true>; phases A and C give every lane two
-//   timesteps (2q, 2q+1) instead of four to half of them.
+// The scan.  With several time segments, the wave of segment s starts from the
+//   copy of h0 that scan_seg_agg leaves in carry plane nseg - 1, folded with the
+//   aggregates of segments 0..s-1 (carry planes 0..s-1).  It never reads h0
+//   itself: the wave of the last segment may then write h_last over h0 while the
+//   waves of earlier segments of the same rows have not started (workgroups are
+//   not ordered).
+// POS = true: also record the states at p.pos (p.npos > 0).
+// CK = true: also store the state at every 16-timestep boundary in p.ck, the
+//   checkpoints the backward recomputes its chunks from.
+// SHORT = true (seqlen 16): one half chunk per wave, with the half-size tables
+//   of WaveSmemT<true>; phases A and C give every lane two timesteps (2q, 2q+1)
+//   instead of four to half of them.
 template <int N> __device__ __forceinline__ void lds_wait() {
     static_assert(N >= 0 && N < 16, "lgkmcnt is a 4-bit field");
     // nothing may be scheduled across the wait, so that the reads issued after
@@ -140,12 +135,11 @@ template <int N> __device__ __forceinline__ void lds_wait() {
     __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool PREPASS, bool POS, bool CK = false,
-          bool SHORT = false>
-__global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len, float *carry) {
+template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool POS, bool CK = false, bool SHORT = false>
+__global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len, const float *carry) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    using Smem = std::conditional_t<PREPASS, WaveSmemPre, WaveSmemT<SHORT>>;
+    using Smem = WaveSmemT<SHORT>;
     Smem &sm = reinterpret_cast<Smem *>(smem_raw)[wave];
     constexpr int kPS = Smem::kSteps / 4;              // part rows per channel
 
@@ -163,15 +157,14 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     const uint32_t blk = blockIdx.x;
     const uint32_t lwg = blk < per_xcd * 8 ? (blk % 8) * per_xcd + blk / 8 : blk;
     const uint32_t wid = lwg * kWavesPerGroup + wave;
-    if (wid >= n_cg * (uint32_t)p.batch * (PREPASS ? nseg - 1 : nseg)) return;   // whole wave leaves together
+    if (wid >= n_cg * (uint32_t)p.batch * nseg) return;   // whole wave leaves together
     // Time segment innermost: the waves resident together work on every segment.
     // Their loads then spread over the L2 sets even when the row stride is a
     // multiple of 128 KB (L = 65536), where the same timestep of every row falls
     // in the same sets: ordered by segment, the 1.6B layer's scan fetched 2.54 GB
     // for 1.81 GB of activations, in this order 1.99 GB.
-    const uint32_t nsg = PREPASS ? nseg - 1 : nseg;
-    const uint32_t rest = wid / nsg;
-    const int64_t seg = wid - rest * nsg;
+    const uint32_t rest = wid / nseg;
+    const int64_t seg = wid - rest * nseg;
     const uint32_t bq = rest / n_cg;
     const int64_t cg = rest - bq * n_cg;
     const int64_t b = bq;
@@ -190,9 +183,9 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
         a2[s] = p.A[dcl * kN + n0 + s] * kLog2e;
-        h[s] = (!PREPASS && nseg == 1 && p.h0) ? p.h0[row * kN + n0 + s] : 0.0f;
+        h[s] = (nseg == 1 && p.h0) ? p.h0[row * kN + n0 + s] : 0.0f;
     }
-    if (!PREPASS && nseg > 1) {
+    if (nseg > 1) {
         // carry-in: the copy of h0 (plane nseg - 1), then the aggregates of the
         // earlier segments; folding (1, h0) into the zero state gives h0 exactly
         auto fold = [&](int64_t plane) {
@@ -203,13 +196,6 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         fold(nseg - 1);
         for (int64_t s2 = 0; s2 < seg; ++s2) fold(s2);
     }
-    if (PREPASS && seg == 0 && live) {
-        const float g0 = p.h0 ? p.h0[row * kN + n0] : 0.0f;
-        const float g1 = p.h0 ? p.h0[row * kN + n0 + 1] : 0.0f;
-        *reinterpret_cast<f32x4 *>(carry + (((int64_t)(nseg - 1) * rows + row) * kN + n0) * 2) =
-            f32x4{1.0f, g0, 1.0f, g1};
-    }
-    float dsum = 0.0f;      // PREPASS: this lane's share of the segment's sum of dlt
     const float dskip = p.Dskip ? p.Dskip[dcl] : 0.0f;
     const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
 
@@ -231,11 +217,9 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     // Elements per lane in phases A and C: timesteps kE q .. kE q + kE - 1.
     constexpr int kE = SHORT ? 2 : 4;
     // B/C staging: lane (j, q) moves timesteps kE j .. kE j + kE - 1 of state
-    // rows 2q and 2q+1 of B and C, i.e. the entries bc[kE j + i][q].  The
-    // pre-pass swaps the roles: timesteps 4q .. 4q+3 of B's state rows 2j and
-    // 2j+1, i.e. the entries b2[2q][j] and b2[2q + 1][j].
-    const int st_t = PREPASS ? 4 * q : kE * j;
-    const uint32_t bc_row = (uint32_t)(2 * (PREPASS ? j : q) * L);
+    // rows 2q and 2q+1 of B and C, i.e. the entries bc[kE j + i][q].
+    const int st_t = kE * j;
+    const uint32_t bc_row = (uint32_t)(2 * q * L);
 
     using Raw = std::conditional_t<SHORT, Raw2<IN>, Raw4<IN>>;
     struct Slot { Raw u, dl, z, B0, B1, C0, C1; };
@@ -248,15 +232,13 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         const uint32_t oa = act_row + ta;
         sl.u.load(ub, oa);
         sl.dl.load(db, oa);
-        if (GATE && !PREPASS) sl.z.load(zb, oa);
+        if (GATE) sl.z.load(zb, oa);
         const uint32_t tb = tr + st_t < seg_n - kE ? tr + st_t : seg_n - kE;
         const uint32_t ob = bc_row + tb;
         sl.B0.load(bb, ob);
         sl.B1.load(bb, ob + (uint32_t)L);
-        if (!PREPASS) {
-            sl.C0.load(cb, ob);
-            sl.C1.load(cb, ob + (uint32_t)L);
-        }
+        sl.C0.load(cb, ob);
+        sl.C1.load(cb, ob + (uint32_t)L);
     };
 
     // Phase B step TQ: timesteps 4 TQ .. 4 TQ + 3, operands already in registers.
@@ -267,31 +249,26 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         for (int k = 0; k < 4; ++k) {
             const float dl = (k & 1) ? ddv[k >> 1].z : ddv[k >> 1].x;
             const float dx = (k & 1) ? ddv[k >> 1].w : ddv[k >> 1].y;
-            const float b0 = PREPASS ? ((k & 1) ? bcv[k >> 1].z : bcv[k >> 1].x) : bcv[k][0];
-            const float b1 = PREPASS ? ((k & 1) ? bcv[k >> 1].w : bcv[k >> 1].y) : bcv[k][1];
+            const float b0 = bcv[k][0];
+            const float b1 = bcv[k][1];
             const float a0 = hw_exp2(dl * a2[0]);
             const float a1 = hw_exp2(dl * a2[1]);
             h[0] = __builtin_fmaf(a0, h[0], dx * b0);
             h[1] = __builtin_fmaf(a1, h[1], dx * b1);
-            if constexpr (!PREPASS) acc4[k] = __builtin_fmaf(bcv[k][3], h[1], bcv[k][2] * h[0]);
+            acc4[k] = __builtin_fmaf(bcv[k][3], h[1], bcv[k][2] * h[0]);
         }
-        if constexpr (!PREPASS) sm.part[kPS * j + TQ][q] = f32x4{acc4[0], acc4[1], acc4[2], acc4[3]};
+        sm.part[kPS * j + TQ][q] = f32x4{acc4[0], acc4[1], acc4[2], acc4[3]};
     };
     auto load4 = [&](f32x4 (&ddv)[2], f32x4 (&bcv)[4], auto tq_c) {
         constexpr int TQ = decltype(tq_c)::value;
 #pragma unroll
         for (int k = 0; k < 2; ++k) ddv[k] = sm.dd[2 * TQ + k][j];
-        if constexpr (PREPASS) {
 #pragma unroll
-            for (int k = 0; k < 2; ++k) bcv[k] = sm.b2[2 * TQ + k][q];
-        } else {
-#pragma unroll
-            for (int k = 0; k < 4; ++k) bcv[k] = sm.bc[4 * TQ + k][q];
-        }
+        for (int k = 0; k < 4; ++k) bcv[k] = sm.bc[4 * TQ + k][q];
     };
     // s_waitcnt lgkmcnt(N) (vmcnt and expcnt left alone): wait until at most N of
     // this wave's LDS operations are outstanding.
-    constexpr int kW = PREPASS ? 0 : 1;      // the scan writes one partial row per step
+    constexpr int kW = 1;      // the scan writes one partial row per step
     // Order this wave's LDS writes before its later reads of other lanes' data.
     auto wave_sync = [] {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -305,7 +282,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     // phase A has not yet rewritten.  The replay repeats phase B's operations
     // in the same order, so the recorded state equals the one the scan carries.
     auto record_positions = [&](int64_t t0, int nt, float r0, float r1) {
-        if constexpr (POS && !PREPASS) for (int64_t k = 0; k < p.npos; ++k) {
+        if constexpr (POS) for (int64_t k = 0; k < p.npos; ++k) {
             const int64_t pk = p.pos[k * p.batch + b];              // wave-uniform
             if (pk < t0 || pk >= t0 + nt) continue;
             const int cnt = (int)(pk - t0) + 1;
@@ -351,26 +328,18 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
                 dl[k] = SOFTPLUS ? softplus_f32(v) : v;
                 dx[k] = dl[k] * x;
                 xs[k] = x;
-                if (GATE && !PREPASS) gs[k] = silu_f32(sl.z.get(k));
+                if (GATE) gs[k] = silu_f32(sl.z.get(k));
             }
             if constexpr (SHORT) {
                 sm.dd[q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
             } else {
                 sm.dd[2 * q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
                 sm.dd[2 * q + 1][j] = f32x4{dl[2], dx[2], dl[3], dx[3]};
-                // pairwise within the quad, then across chunks and lanes: the
-                // rounding of the segment's sum stays small
-                if (PREPASS && 4 * q < nt) dsum += (dl[0] + dl[1]) + (dl[2] + dl[3]);
             }
         }
-        if constexpr (PREPASS) {
-            sm.b2[2 * q][j] = f32x4{sl.B0.get(0), sl.B1.get(0), sl.B0.get(1), sl.B1.get(1)};
-            sm.b2[2 * q + 1][j] = f32x4{sl.B0.get(2), sl.B1.get(2), sl.B0.get(3), sl.B1.get(3)};
-        } else {
 #pragma unroll
-            for (int k = 0; k < kE; ++k)
-                sm.bc[st_t + k][q] = f32x4{sl.B0.get(k), sl.B1.get(k), sl.C0.get(k), sl.C1.get(k)};
-        }
+        for (int k = 0; k < kE; ++k)
+            sm.bc[st_t + k][q] = f32x4{sl.B0.get(k), sl.B1.get(k), sl.C0.get(k), sl.C1.get(k)};
         wave_sync();
 
         // refill this slot with the chunk after next while the recurrence runs
@@ -429,60 +398,58 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         }
         wave_sync();
 
-        if constexpr (!PREPASS) {
-            // ---- C: sum the 8 partials of channel j at timesteps 2q, 2q+1 ----------
-            if constexpr (SHORT) {
-                // the partials of timesteps 2q, 2q+1 are one half of entry (j, q >> 1)
-                const float2 *src = reinterpret_cast<const float2 *>(&sm.part[kPS * j + (q >> 1)][0]) + (q & 1);
-                float2 acc = src[0];
+        // ---- C: sum the 8 partials of channel j at timesteps 2q, 2q+1 ----------
+        if constexpr (SHORT) {
+            // the partials of timesteps 2q, 2q+1 are one half of entry (j, q >> 1)
+            const float2 *src = reinterpret_cast<const float2 *>(&sm.part[kPS * j + (q >> 1)][0]) + (q & 1);
+            float2 acc = src[0];
 #pragma unroll
-                for (int w = 1; w < kQ; ++w) {
-                    acc.x += src[2 * w].x;
-                    acc.y += src[2 * w].y;
-                }
-                float yv[2];
+            for (int w = 1; w < kQ; ++w) {
+                acc.x += src[2 * w].x;
+                acc.y += src[2 * w].y;
+            }
+            float yv[2];
 #pragma unroll
-                for (int k = 0; k < 2; ++k) {
-                    float y = __builtin_fmaf(dskip, xs[k], k ? acc.y : acc.x);
+            for (int k = 0; k < 2; ++k) {
+                float y = __builtin_fmaf(dskip, xs[k], k ? acc.y : acc.x);
+                if (GATE) y *= gs[k];
+                yv[k] = y;
+            }
+            if (live) {
+                const uint32_t oy = act_row + (uint32_t)(t0 - t_begin) + 2 * q;
+                if (OUT == 0)
+                    *reinterpret_cast<float2 *>(yb + oy * 4u) = float2{yv[0], yv[1]};
+                else
+                    *reinterpret_cast<uint32_t *>(yb + oy * 2u) =
+                        (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
+            }
+        } else {
+            if (4 * q < nt) {
+                // ---- C: sum the 8 partials of channel j at timesteps 4q .. 4q+3 ----
+                f32x4 acc = sm.part[kPS * j + q][0];
+#pragma unroll
+                for (int w = 1; w < kQ; ++w) acc += sm.part[kPS * j + q][w];
+                float yv[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    float y = __builtin_fmaf(dskip, xs[k], acc[k]);
                     if (GATE) y *= gs[k];
                     yv[k] = y;
                 }
                 if (live) {
-                    const uint32_t oy = act_row + (uint32_t)(t0 - t_begin) + 2 * q;
-                    if (OUT == 0)
-                        *reinterpret_cast<float2 *>(yb + oy * 4u) = float2{yv[0], yv[1]};
-                    else
-                        *reinterpret_cast<uint32_t *>(yb + oy * 2u) =
-                            (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
-                }
-            } else {
-                if (4 * q < nt) {
-                    // ---- C: sum the 8 partials of channel j at timesteps 4q .. 4q+3 ----
-                    f32x4 acc = sm.part[kPS * j + q][0];
-#pragma unroll
-                    for (int w = 1; w < kQ; ++w) acc += sm.part[kPS * j + q][w];
-                    float yv[4];
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        float y = __builtin_fmaf(dskip, xs[k], acc[k]);
-                        if (GATE) y *= gs[k];
-                        yv[k] = y;
-                    }
-                    if (live) {
-                        const uint32_t oy = act_row + (uint32_t)(t0 - t_begin) + 4 * q;
-                        if (OUT == 0) {
-                            *reinterpret_cast<f32x4 *>(yb + oy * 4u) = f32x4{yv[0], yv[1], yv[2], yv[3]};
-                        } else {
-                            const uint32_t w0 = (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
-                            const uint32_t w1 = (uint32_t)f32_to_bf16(yv[2]) | ((uint32_t)f32_to_bf16(yv[3]) << 16);
-                            *reinterpret_cast<u32x2 *>(yb + oy * 2u) = u32x2{w0, w1};
-                        }
+                    const uint32_t oy = act_row + (uint32_t)(t0 - t_begin) + 4 * q;
+                    if (OUT == 0) {
+                        *reinterpret_cast<f32x4 *>(yb + oy * 4u) = f32x4{yv[0], yv[1], yv[2], yv[3]};
+                    } else {
+                        const uint32_t w0 = (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
+                        const uint32_t w1 = (uint32_t)f32_to_bf16(yv[2]) | ((uint32_t)f32_to_bf16(yv[3]) << 16);
+                        *reinterpret_cast<u32x2 *>(yb + oy * 2u) = u32x2{w0, w1};
                     }
                 }
             }
-            if (POS) record_positions(t0, nt, hs0, hs1);
-            wave_sync();   // part / dd / bc are rewritten by the next chunk
         }
+        if (POS) record_positions(t0, nt, hs0, hs1);
+        wave_sync();   // part / dd / bc are rewritten by the next chunk
     };
 
     issue_loads(s0, 0);
@@ -499,19 +466,192 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         if (t0 + kT < t_end) chunk(s1, t0 + kT);
     }
 
-    if constexpr (PREPASS) {
-        // the eight lanes of channel j hold its timesteps 4q .. 4q+3 of every
-        // chunk: after the butterfly each holds the whole segment's sum
-        dsum += __shfl_xor(dsum, 1);
-        dsum += __shfl_xor(dsum, 2);
-        dsum += __shfl_xor(dsum, 4);
-        if (live) {
-            const float P0 = hw_exp2(a2[0] * dsum), P1 = hw_exp2(a2[1] * dsum);
-            *reinterpret_cast<f32x4 *>(carry + ((seg * rows + row) * kN + n0) * 2) = f32x4{P0, h[0], P1, h[1]};
-        }
-    } else if (p.h_last && live && seg == nseg - 1) {
+    if (p.h_last && live && seg == nseg - 1) {
 #pragma unroll
         for (int s = 0; s < 2; ++s) p.h_last[row * kN + n0 + s] = h[s];
+    }
+}
+
+// ---- segment aggregates ------------------------------------------------------
+//
+// For every time segment but the last (seg_len timesteps, a multiple of 32) and
+// every state n of a row, the segment's element of the associative operator of
+// Section 2 ("Implementation"):
+//   P[n] = prod_t abar_t[n] = 2^(A[n] log2 e sum_t dlt_t),
+//   H[n] = sum_t (prod_{r > t} abar_r[n]) dlt_t B_t[n] x_t,
+// so that the state at the segment's end is P h_start + H.  H is the state the
+// recurrence reaches from a zero state at the segment's start; P is one
+// exponential of the segment's summed dlt, not a product of hundreds of
+// hardware exponentials near 1, whose rounding would drift and be carried into
+// every later segment by the fold P h + H.  The pairs (P, H) go to
+// carry[((seg * rows + row) * 16 + n) * 2 + {0, 1}].
+//
+// A walk from the segment's end that stops once the running product of abar is
+// exactly zero in fp32 gives the same (P, H) with fewer timesteps, but with the
+// timestep bias of the MambaByte layers (dt down to 1e-3) some channel of almost
+// every 8-channel wave decays too slowly for that within a segment, and the walk
+// costs a multiply more per step: measured slower on the 1.6B layer.
+//
+// The waves of segment 0 also copy h0 (or zeros) into plane nseg - 1 as the pairs
+// (1, h0[n]), which the scan folds first.
+//
+// Lane l = 8 j + q as in the scan: channel j, states 2q and 2q+1.  Per chunk,
+// lane (j, q) forms dlt and dx of channel j at timesteps 4q .. 4q+3 and stages B
+// rows 2j and 2j+1 at those timesteps (the dd and b2 tables of WaveSmemPre).
+template <int IN, bool SOFTPLUS>
+__global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t seg_len, float *carry) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    WaveSmemPre &sm = reinterpret_cast<WaveSmemPre *>(smem_raw)[wave];
+
+    const int lane = threadIdx.x & 63;
+    const int j = lane >> 3;
+    const int q = lane & 7;
+    const uint32_t n_cg = (uint32_t)((p.dim + kCh - 1) / kCh);
+    const uint32_t nseg = ((uint32_t)p.seqlen + (uint32_t)seg_len - 1) / (uint32_t)seg_len;
+    const uint32_t nsg = nseg - 1;                      // the segments that have an aggregate
+    const uint32_t per_xcd = gridDim.x / 8;
+    const uint32_t blk = blockIdx.x;
+    const uint32_t lwg = blk < per_xcd * 8 ? (blk % 8) * per_xcd + blk / 8 : blk;
+    const uint32_t wid = lwg * kWavesPerGroup + wave;
+    if (wid >= n_cg * (uint32_t)p.batch * nsg) return;   // whole wave leaves together
+    const uint32_t rest = wid / nsg;
+    const int64_t seg = wid - rest * nsg;
+    const uint32_t bq = rest / n_cg;
+    const int64_t cg = rest - bq * n_cg;
+    const int64_t b = bq;
+    const int64_t t_begin = seg * seg_len;
+
+    const int64_t d = cg * kCh + j;
+    const bool live = d < p.dim;
+    const int64_t dcl = live ? d : p.dim - 1;           // dead lanes read a valid row, never store
+    const int64_t row = b * p.dim + dcl;
+    const int64_t L = p.seqlen;
+    const int n0 = 2 * q;
+    const int64_t rows = p.batch * p.dim;
+
+    float a2[2], h[2] = {0.0f, 0.0f};
+    float dsum = 0.0f;      // this lane's share of the segment's sum of dlt
+#pragma unroll
+    for (int s = 0; s < 2; ++s) a2[s] = p.A[dcl * kN + n0 + s] * kLog2e;
+    if (seg == 0 && live) {
+        const float g0 = p.h0 ? p.h0[row * kN + n0] : 0.0f;
+        const float g1 = p.h0 ? p.h0[row * kN + n0 + 1] : 0.0f;
+        *reinterpret_cast<f32x4 *>(carry + (((int64_t)nsg * rows + row) * kN + n0) * 2) =
+            f32x4{1.0f, g0, 1.0f, g1};
+    }
+    const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
+
+    constexpr int kEl = IN == 1 ? 2 : 4;
+    const int64_t row0 = b * p.dim + cg * kCh;                       // wave-uniform
+    const int64_t act0 = row0 * L + t_begin;
+    const char *ub = static_cast<const char *>(p.u) + act0 * kEl;
+    const char *db = static_cast<const char *>(p.delta) + act0 * kEl;
+    const char *bb = static_cast<const char *>(p.Bm) + (b * kN * L + t_begin) * kEl;
+    const uint32_t act_row = (uint32_t)((dcl - cg * kCh) * L);       // lane's channel row
+    const uint32_t bc_row = (uint32_t)(2 * j * L);                   // B rows 2j, 2j+1
+    const uint32_t nch = (uint32_t)(seg_len / kT);
+
+    struct Slot { Raw4<IN> u, dl, B0, B1; };
+    Slot s0, s1;
+    // Chunk k starts at 32 k; past the segment's end the loads read the last
+    // chunk again (never consumed).
+    auto issue_loads = [&](Slot &sl, uint32_t k) {
+        const uint32_t tr = (k < nch ? k : nch - 1) * kT + 4 * q;
+        sl.u.load(ub, act_row + tr);
+        sl.dl.load(db, act_row + tr);
+        sl.B0.load(bb, bc_row + tr);
+        sl.B1.load(bb, bc_row + tr + (uint32_t)L);
+    };
+    // Four timesteps: table rows 2 TQ and 2 TQ + 1, the even timestep of a row first.
+    auto fwd4 = [&](const f32x4 (&dv)[2], const f32x4 (&bv)[2]) {
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+#pragma unroll
+            for (int o = 0; o < 2; ++o) {
+                const float dl = o ? dv[k].z : dv[k].x;
+                const float dx = o ? dv[k].w : dv[k].y;
+                const float b0 = o ? bv[k].z : bv[k].x;
+                const float b1 = o ? bv[k].w : bv[k].y;
+                h[0] = __builtin_fmaf(hw_exp2(dl * a2[0]), h[0], dx * b0);
+                h[1] = __builtin_fmaf(hw_exp2(dl * a2[1]), h[1], dx * b1);
+            }
+        }
+    };
+    auto load2 = [&](f32x4 (&dv)[2], f32x4 (&bv)[2], int tq) {
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            dv[k] = sm.dd[2 * tq + k][j];
+            bv[k] = sm.b2[2 * tq + k][q];
+        }
+    };
+    auto wave_sync = [] {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    };
+
+    auto chunk = [&](Slot &sl, uint32_t k) {
+        float dl[4], dx[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float v = sl.dl.get(i) + bias;
+            dl[i] = SOFTPLUS ? softplus_f32(v) : v;
+            dx[i] = dl[i] * sl.u.get(i);
+        }
+        // pairwise within the quad, then across chunks and lanes: the rounding
+        // of the segment's sum stays small
+        dsum += (dl[0] + dl[1]) + (dl[2] + dl[3]);
+        sm.dd[2 * q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
+        sm.dd[2 * q + 1][j] = f32x4{dl[2], dx[2], dl[3], dx[3]};
+        sm.b2[2 * q][j] = f32x4{sl.B0.get(0), sl.B1.get(0), sl.B0.get(1), sl.B1.get(1)};
+        sm.b2[2 * q + 1][j] = f32x4{sl.B0.get(2), sl.B1.get(2), sl.B0.get(3), sl.B1.get(3)};
+        wave_sync();
+        issue_loads(sl, k + 2);
+        {
+            f32x4 dA[2], bA[2], dB[2], bB[2];
+            load2(dA, bA, 0);
+            lds_wait<0>();
+            load2(dB, bB, 1);
+            fwd4(dA, bA);
+            lds_wait<0>();
+            load2(dA, bA, 2);
+            fwd4(dB, bB);
+            lds_wait<0>();
+            load2(dB, bB, 3);
+            fwd4(dA, bA);
+            lds_wait<0>();
+            load2(dA, bA, 4);
+            fwd4(dB, bB);
+            lds_wait<0>();
+            load2(dB, bB, 5);
+            fwd4(dA, bA);
+            lds_wait<0>();
+            load2(dA, bA, 6);
+            fwd4(dB, bB);
+            lds_wait<0>();
+            load2(dB, bB, 7);
+            fwd4(dA, bA);
+            lds_wait<0>();
+            fwd4(dB, bB);
+        }
+        wave_sync();                                  // dd / b2 are rewritten by the next chunk
+    };
+
+    issue_loads(s0, 0);
+    issue_loads(s1, 1);
+    for (uint32_t k = 0; k < nch; k += 2) {
+        chunk(s0, k);
+        if (k + 1 < nch) chunk(s1, k + 1);
+    }
+    // the eight lanes of channel j hold its timesteps 4q .. 4q+3 of every chunk:
+    // after the butterfly each holds the whole segment's sum
+    dsum += __shfl_xor(dsum, 1);
+    dsum += __shfl_xor(dsum, 2);
+    dsum += __shfl_xor(dsum, 4);
+    if (live) {
+        const float P0 = hw_exp2(a2[0] * dsum), P1 = hw_exp2(a2[1] * dsum);
+        *reinterpret_cast<f32x4 *>(carry + ((seg * rows + row) * kN + n0) * 2) = f32x4{P0, h[0], P1, h[1]};
     }
 }
 
@@ -586,9 +726,8 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream, float *lent) {
         const int64_t waves = n_cg * p.batch * (nseg - 1);
         const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;
         void *args[] = {&p, &seg_len, &carry};
-        e = hipLaunchKernel(reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, true, false>),
-                            dim3((unsigned)blocks), dim3(kThreads), args,
-                            sizeof(WaveSmemPre) * kWavesPerGroup, st);
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&scan_seg_agg<IN, SP>), dim3((unsigned)blocks),
+                            dim3(kThreads), args, sizeof(WaveSmemPre) * kWavesPerGroup, st);
         if (e != hipSuccess) {
             if (!lent) (void)hipFreeAsync(carry, st);
             return e;
@@ -601,11 +740,11 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream, float *lent) {
     const bool short_seq = p.seqlen == kT / 2 && nseg == 1 && !p.ck;
     const void *main_fn =
         short_seq ? (p.npos > 0
-                         ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, true, false, true>)
-                         : reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false, false, true>))
-        : p.npos > 0 ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, true>)
-        : p.ck       ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false, true>)
-                     : reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false>);
+                         ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, true, false, true>)
+                         : reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, false, true>))
+        : p.npos > 0 ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, true>)
+        : p.ck       ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, true>)
+                     : reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false>);
     const size_t main_lds = short_seq ? sizeof(WaveSmemT<true>) * kWavesPerGroup : lds;
     e = hipLaunchKernel(main_fn, dim3((unsigned)blocks), dim3(kThreads), args, main_lds, st);
     if (carry && !lent) {
