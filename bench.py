@@ -26,18 +26,26 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, 8 TB/s
 
 # Issue model of the scan, reported beside the HBM roofline (which is the
-# roofline of record).  Rates measured on MI355X by a micro-benchmark (kernel time
-# from events over a grid with W waves on every SIMD, shader clock read in the
-# kernel): a plain two-operand fp32 VALU instruction (v_mul_f32, v_add_f32,
-# v_fmac_f32) holds its SIMD for 2.24 cycles with 8 waves per SIMD (2.5 with 2,
-# 4.9 with 1: only interleaved waves reach the dual-issue rate); a transcendental
-# (v_exp_f32, v_log_f32, v_rcp_f32) holds it for 8.1 cycles at any occupancy, and
-# the two do not overlap.  Per element the forward needs at least 76 VALU and 20
-# transcendental lane-operations: per state dlt * A, its exponential, dlt * u * B,
-# the state FMA and the C FMA (64 + 16), and per element softplus (exp, log),
-# silu (exp, rcp) and about 12 VALU operations.  At the best rates and 2.4 GHz
-# that is 5.2 SIMD-cycles per element.
-VALU_CYCLES, TRANS_CYCLES = 2.24, 8.13
+# roofline of record).  Rates measured on MI355X by paper_2401_13660_amd/issue_rates
+# (csrc/issue_rates.hip; register-only instruction streams, kernel time from events
+# over a grid with W waves on every SIMD, shader clock read in the kernel):
+#  - a transcendental (v_exp_f32) holds its SIMD for 8.0-9.2 cycles at any
+#    occupancy (8.6 with 2 waves per SIMD) and no other VALU instruction issues
+#    meanwhile, not even from another wave;
+#  - other fp32 VALU instructions reach 2.3-2.5 cycles with two or more waves per
+#    SIMD only in streams without transcendentals (two waves issue in the same
+#    cycle; one wave alone issues one about every 7 cycles), and only when no
+#    operand is an SGPR and the two multiplicand VGPRs of a multiply-add differ in
+#    parity (index mod 2);
+#  - with one transcendental per four other instructions, as in the scan, and 2
+#    waves per SIMD (the scan's occupancy), the mix averages 5.0 cycles per
+#    instruction: 8.6 for the exponential and 4.1 for each of the others.
+# Per element the forward needs at least 76 VALU and 20 transcendental
+# lane-operations: per state dlt * A, its exponential, dlt * u * B, the state FMA
+# and the C FMA (64 + 16), and per element softplus (exp, log), silu (exp, rcp) and
+# about 12 VALU operations.  At those rates and 2.4 GHz that is 7.6 SIMD-cycles per
+# element.
+VALU_CYCLES, TRANS_CYCLES = 4.1, 8.6
 ALU_SIMD_CYCLES_PER_ELEMENT = (76 * VALU_CYCLES + 20 * TRANS_CYCLES) / 64.0
 ALU_PEAK_GELEMS = 1024 * 2.4e9 / ALU_SIMD_CYCLES_PER_ELEMENT / 1e9
 # The same model for the backward (the gradients of eq. (2) by reverse-mode
@@ -669,8 +677,8 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": traffic, "algorithmic_bytes": nbytes,
                      "scope": "whole step (all kernels of one call)"},
-        # secondary: the same step against the issue model (VALU 2.24, transcendental
-        # 8.13 SIMD-cycles per wave64 instruction; 76 + 20 per element; 2.4 GHz)
+        # secondary: the same step against the issue model (VALU 4.1, transcendental
+        # 8.6 SIMD-cycles per wave64 instruction; 76 + 20 per element; 2.4 GHz)
         "alu_model": {"achieved": round(E / (ms * 1e-3) / 1e9, 2), "peak": round(ALU_PEAK_GELEMS, 1),
                       "unit": "Gelem/s", "frac": round(E / (ms * 1e-3) / 1e9 / ALU_PEAK_GELEMS, 4)},
     }

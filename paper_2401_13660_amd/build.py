@@ -1,4 +1,5 @@
-"""Build the HIP library libmbscan.so in-tree (gfx950 only).
+"""Build the HIP library libmbscan.so in-tree (gfx950 only), and the issue-rate
+micro-benchmark behind the instruction cost model (csrc/issue_rates.hip).
 
     python -m paper_2401_13660_amd.build
 """
@@ -13,6 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libmbscan.so")
 SOURCES = ["mbscan.hip"]
+ISSUE_RATES = os.path.join(PKG, "issue_rates")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -37,7 +39,23 @@ def build(verbose: bool = False) -> str:
         sys.stderr.write(res.stdout + res.stderr)
         raise RuntimeError("hipcc failed to build libmbscan.so")
     os.replace(tmp, LIB)
+    build_issue_rates(verbose)
     return LIB
+
+
+def build_issue_rates(verbose: bool = False) -> str:
+    """The stand-alone issue-rate program (run it on the GPU: ./issue_rates)."""
+    tmp = ISSUE_RATES + ".tmp"
+    flags = [f for f in FLAGS if f not in ("-fPIC", "-shared")]
+    cmd = [HIPCC, *flags, os.path.join(CSRC, "issue_rates.hip"), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd))
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError("hipcc failed to build issue_rates")
+    os.replace(tmp, ISSUE_RATES)
+    return ISSUE_RATES
 
 
 if __name__ == "__main__":
