@@ -640,10 +640,12 @@ __global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t s
 
     issue_loads(s0, 0);
     issue_loads(s1, 1);
-    for (uint32_t k = 0; k < nch; k += 2) {
+    uint32_t k = 0;
+    for (; k + 2 <= nch; k += 2) {                  // pairs of chunks
         chunk(s0, k);
-        if (k + 1 < nch) chunk(s1, k + 1);
+        chunk(s1, k + 1);
     }
+    if (k < nch) chunk(s0, k);                      // an odd chunk count leaves one
     // the eight lanes of channel j hold its timesteps 4q .. 4q+3 of every chunk:
     // after the butterfly each holds the whole segment's sum
     dsum += __shfl_xor(dsum, 1);
