@@ -149,7 +149,8 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     // Wave indexing in 32 bits: the host launches fewer than 2^31 waves and
     // sends sequences shorter than 2^25 bytes here, so every quotient below fits.
     const uint32_t n_cg = (uint32_t)((p.dim + kCh - 1) / kCh);
-    const uint32_t nseg = ((uint32_t)p.seqlen + (uint32_t)seg_len - 1) / (uint32_t)seg_len;
+    // (a 16-byte sequence is never cut into time segments: no division for it)
+    const uint32_t nseg = SHORT ? 1u : ((uint32_t)p.seqlen + (uint32_t)seg_len - 1) / (uint32_t)seg_len;
     // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2);
     // renumber them so that an XCD works on a contiguous range of (batch,
     // channel) groups and the B/C rows of a batch stay in one or two L2s.
