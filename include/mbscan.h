@@ -199,6 +199,9 @@ int mb_scan_fwd_ckpt(const mb_scan_desc *desc,
  *   z_t            act   (B, D)     NULL means no gate
  *   h              float (B, D, N)  state, read then overwritten; required
  *   y_t            out   (B, D)     output; must not overlap any input or h
+ *
+ * dim must stay below 2^36 (the launch covers 64 channels per workgroup along
+ * one grid dimension); a larger one returns MB_ERR_SHAPE.
  */
 int mb_scan_step(int64_t batch, int64_t dim, int64_t dstate,
                  int32_t in_dtype, int32_t out_dtype, int32_t delta_softplus,

@@ -95,9 +95,9 @@ hipError_t fwd_dispatch_n(ScanParams &p, int64_t N, void *stream, float *lent) {
 
 template <int IN, int OUT, int N>
 hipError_t step_launch(StepParams &p, void *stream) {
-    constexpr int lanes = N >= 4 ? 4 : 1;
-    const int64_t threads = p.batch * p.dim * lanes;
-    const dim3 block(256), grid((unsigned)((threads + 255) / 256));
+    constexpr int64_t per_block = mbs::kStepRowsPerBlock<N>;
+    const dim3 block(256);
+    const dim3 grid((unsigned)((p.dim + per_block - 1) / per_block), (unsigned)(p.batch < 65535 ? p.batch : 65535));
     return launch(reinterpret_cast<const void *>(&mbs::scan_step_kernel<IN, OUT, N>), grid, block, &p,
                   stream);
 }
@@ -730,7 +730,8 @@ int mb_scan_step(int64_t batch, int64_t dim, int64_t dstate, int32_t in_dtype, i
                  int32_t delta_softplus, const void *u_t, const void *delta_t, const float *A,
                  const void *B_t, const void *C_t, const float *Dskip, const float *dt_bias,
                  const void *z_t, float *h, void *y_t, void *stream) {
-    if (batch < 0 || dim < 0 || dstate < 0) return MB_ERR_SHAPE;
+    // dim below 2^36: at most 2^30 channel blocks of 64 along the grid's x
+    if (batch < 0 || dim < 0 || dstate < 0 || dim >= (int64_t(1) << 36)) return MB_ERR_SHAPE;
     if (!valid_dtype(in_dtype) || !valid_dtype(out_dtype)) return MB_ERR_DTYPE;
     if (!supported_dstate(dstate)) return MB_ERR_UNSUPPORTED;
     int64_t rows, state_elems, bc_elems;

@@ -11,62 +11,72 @@
 
 namespace mbs {
 
+// Launch: 256-thread blocks, grid.x = ceil(dim / (256 / lanes)) channel blocks,
+// grid.y = min(batch, 65535); each block steps its channels for batch elements
+// blockIdx.y, blockIdx.y + gridDim.y, ...  No thread divides: the channel and the
+// lane's share of the states come from the thread index by shifts.
+template <int N> constexpr int kStepLanes = N >= 4 ? 4 : 1;      // lanes per row
+template <int N> constexpr int kStepRowsPerBlock = 256 / kStepLanes<N>;
+
 template <int IN, int OUT, int N>
 __global__ __launch_bounds__(256) void scan_step_kernel(StepParams p) {
-    constexpr int LANES = N >= 4 ? 4 : 1;      // lanes per row
+    constexpr int LANES = kStepLanes<N>;
     constexpr int S = N / LANES;               // states per lane
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t rows = p.batch * p.dim;
-    const int64_t row = gid / LANES;
-    const int part = (int)(gid - row * LANES);
-    const bool live = row < rows;
-    const int64_t r = live ? row : 0;           // dead lanes still take part in the shuffles
-    const int64_t b = r / p.dim;
-    const int64_t d = r - b * p.dim;
-
-    // Every load is issued before the first use of any of them, so that a step
-    // costs one round trip to memory instead of three (activations, then state,
-    // then gate).  An absent optional input reads a stand-in of the same size
-    // (u for z, A for Dskip and dt_bias) and its value is discarded, so no load
-    // sits in a branch that would wait for it.  The 4 lanes of a row read the
-    // same activation words.
-    float hs[S], av[S], bv[S], cv[S];
+    const int tid = threadIdx.x;
+    const int part = tid % LANES;
+    const int64_t d = (int64_t)blockIdx.x * kStepRowsPerBlock<N> + tid / LANES;
+    const bool dlive = d < p.dim;
+    const int64_t dc = dlive ? d : 0;          // dead lanes still take part in the shuffles
+    // per channel: A, and the optional bias and skip (an absent one reads a
+    // stand-in of the same size, A, whose value is discarded)
+    float av[S];
 #pragma unroll
-    for (int s = 0; s < S; ++s) {
-        const int n = part * S + s;
-        hs[s] = p.h[r * N + n];
-        av[s] = p.A[d * N + n];
-        bv[s] = Act<IN>::ld(p.Bt, b * N + n);
-        cv[s] = Act<IN>::ld(p.Ct, b * N + n);
-    }
-    const float x = Act<IN>::ld(p.u, r);
-    const float draw = Act<IN>::ld(p.delta, r);
-    const float bias_raw = (p.dt_bias ? p.dt_bias : p.A)[d];
-    const float z_raw = Act<IN>::ld(p.z ? p.z : p.u, r);
-    const float dskip_raw = (p.Dskip ? p.Dskip : p.A)[d];
+    for (int s = 0; s < S; ++s) av[s] = p.A[dc * N + part * S + s] * kLog2e;
+    const float bias_raw = (p.dt_bias ? p.dt_bias : p.A)[dc];
+    const float dskip_raw = (p.Dskip ? p.Dskip : p.A)[dc];
     const float bias = p.dt_bias ? bias_raw : 0.0f;
     const float dskip = p.Dskip ? dskip_raw : 0.0f;
-    const float v = draw + bias;
-    const float dlt = p.delta_softplus ? softplus_f32(v) : v;
-    const float dx = dlt * x;
-    float acc = 0.0f;
+
+    for (int64_t b = blockIdx.y; b < p.batch; b += gridDim.y) {
+        const int64_t r = b * p.dim + dc;
+        // Every load is issued before the first use of any of them, so that a
+        // step costs one round trip to memory instead of three (activations, then
+        // state, then gate).  An absent gate reads u instead, discarded.  The
+        // lanes of a row read the same activation words.
+        float hs[S], bv[S], cv[S];
 #pragma unroll
-    for (int s = 0; s < S; ++s) {
-        const float abar = hw_exp2(dlt * (av[s] * kLog2e));
-        hs[s] = __builtin_fmaf(abar, hs[s], dx * bv[s]);
-        acc = __builtin_fmaf(cv[s], hs[s], acc);
-    }
-    if (LANES == 4) {
-        acc += __shfl_xor(acc, 1, 4);
-        acc += __shfl_xor(acc, 2, 4);
-    }
-    if (!live) return;
+        for (int s = 0; s < S; ++s) {
+            const int n = part * S + s;
+            hs[s] = p.h[r * N + n];
+            bv[s] = Act<IN>::ld(p.Bt, b * N + n);
+            cv[s] = Act<IN>::ld(p.Ct, b * N + n);
+        }
+        const float x = Act<IN>::ld(p.u, r);
+        const float draw = Act<IN>::ld(p.delta, r);
+        const float z_raw = Act<IN>::ld(p.z ? p.z : p.u, r);
+        const float v = draw + bias;
+        const float dlt = p.delta_softplus ? softplus_f32(v) : v;
+        const float dx = dlt * x;
+        float acc = 0.0f;
 #pragma unroll
-    for (int s = 0; s < S; ++s) p.h[r * N + part * S + s] = hs[s];
-    if (part == 0) {
-        float yv = __builtin_fmaf(dskip, x, acc);
-        if (p.z) yv *= silu_f32(z_raw);
-        st_out<OUT>(p.y, r, yv);
+        for (int s = 0; s < S; ++s) {
+            const float abar = hw_exp2(dlt * av[s]);
+            hs[s] = __builtin_fmaf(abar, hs[s], dx * bv[s]);
+            acc = __builtin_fmaf(cv[s], hs[s], acc);
+        }
+        if (LANES == 4) {
+            acc += __shfl_xor(acc, 1, 4);
+            acc += __shfl_xor(acc, 2, 4);
+        }
+        if (dlive) {
+#pragma unroll
+            for (int s = 0; s < S; ++s) p.h[r * N + part * S + s] = hs[s];
+            if (part == 0) {
+                float yv = __builtin_fmaf(dskip, x, acc);
+                if (p.z) yv *= silu_f32(z_raw);
+                st_out<OUT>(p.y, r, yv);
+            }
+        }
     }
 }
 

@@ -283,6 +283,7 @@ def test_step_rejects():
     f = lib.mb_scan_step
     ok = [P["u"], P["delta"], P["A"], P["B"], P["C"], P["D"], P["bias"], P["z"], P["h0"], P["y"], None]
     assert f(-1, 8, 16, 1, 0, 1, *ok) == -2
+    assert f(1, 1 << 36, 16, 1, 0, 1, *ok) == -2         # dim at the launch bound (2^36)
     assert f(2, 8, 12, 1, 0, 1, *ok) == -5
     assert f(2, 8, 16, 4, 0, 1, *ok) == -3
     bad = list(ok); bad[8] = None                       # h is required
