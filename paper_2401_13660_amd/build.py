@@ -1,5 +1,6 @@
-"""Build the HIP library libmbscan.so in-tree (gfx950 only), and the issue-rate
-micro-benchmark behind the instruction cost model (csrc/issue_rates.hip).
+"""Build the HIP library libmbscan.so in-tree (gfx950 only), the issue-rate
+micro-benchmark behind the instruction cost model (csrc/issue_rates.hip), and
+the exhaustive check of the bf16 pair conversion (csrc/bf16_pack_check.hip).
 
     python -m paper_2401_13660_amd.build
 """
@@ -14,7 +15,6 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libmbscan.so")
 SOURCES = ["mbscan.hip"]
-ISSUE_RATES = os.path.join(PKG, "issue_rates")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -40,23 +40,34 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed to build libmbscan.so")
     os.replace(tmp, LIB)
     build_issue_rates(verbose)
+    build_bf16_pack_check(verbose)
     return LIB
 
 
-def build_issue_rates(verbose: bool = False) -> str:
-    """The stand-alone issue-rate program (run it on the GPU: ./issue_rates)."""
-    tmp = ISSUE_RATES + ".tmp"
+def build_tool(name: str, verbose: bool = False) -> str:
+    """A stand-alone GPU program from csrc/<name>.hip, as paper_2401_13660_amd/<name>."""
+    out = os.path.join(PKG, name)
+    tmp = out + ".tmp"
     flags = [f for f in FLAGS if f not in ("-fPIC", "-shared")]
-    cmd = [HIPCC, *flags, os.path.join(CSRC, "issue_rates.hip"), "-o", tmp]
+    cmd = [HIPCC, *flags, "-I", CSRC, os.path.join(CSRC, name + ".hip"), "-o", tmp]
     if verbose:
         print(" ".join(cmd))
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("hipcc failed to build issue_rates")
-    os.replace(tmp, ISSUE_RATES)
-    return ISSUE_RATES
+        raise RuntimeError(f"hipcc failed to build {name}")
+    os.replace(tmp, out)
+    return out
 
+
+def build_issue_rates(verbose: bool = False) -> str:
+    """The stand-alone issue-rate program (run it on the GPU: ./issue_rates)."""
+    return build_tool("issue_rates", verbose)
+
+
+def build_bf16_pack_check(verbose: bool = False) -> str:
+    """The exhaustive check of the bf16 pair conversion (run by a GPU test)."""
+    return build_tool("bf16_pack_check", verbose)
 
 if __name__ == "__main__":
     print(build(verbose=True))

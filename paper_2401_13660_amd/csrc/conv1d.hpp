@@ -61,7 +61,7 @@ template <> __device__ __forceinline__ void store8<1>(void *base, int64_t off, c
     u32x4 r;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-        r[i] = (uint32_t)f32_to_bf16(v[2 * i]) | ((uint32_t)f32_to_bf16(v[2 * i + 1]) << 16);
+        r[i] = bf16x2_pack(v[2 * i], v[2 * i + 1]);
     *reinterpret_cast<u32x4 *>(static_cast<uint16_t *>(base) + off) = r;
 }
 template <> __device__ __forceinline__ void store8<0>(void *base, int64_t off, const float (&v)[kSpan]) {

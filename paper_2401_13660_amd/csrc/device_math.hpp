@@ -29,6 +29,16 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
     return (uint16_t)(x >> 16);
 }
 
+// Two floats rounded to bfloat16 and packed, a in the low half: one
+// v_cvt_pk_bf16_f32 on gfx950.  It rounds to nearest even and keeps a NaN a quiet
+// NaN with its sign, so it gives f32_to_bf16's bits for every fp32 pattern
+// (bf16_pack_check.hip compares the two over all 2^32 of them on the GPU).
+__device__ __forceinline__ uint32_t bf16x2_pack(float a, float b) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
+}
+
 // Hardware transcendentals: v_exp_f32 = 2^x, v_log_f32 = log2 x, v_rcp_f32 = 1/x.
 __device__ __forceinline__ float hw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float hw_log2(float x) { return __builtin_amdgcn_logf(x); }

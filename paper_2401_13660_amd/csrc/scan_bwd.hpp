@@ -111,7 +111,7 @@ template <int DT> __device__ __forceinline__ void store2(const char *base, uint3
     if (DT == 0) {
         *reinterpret_cast<u32x2 *>(at) = u32x2{__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b)};
     } else {
-        *reinterpret_cast<uint32_t *>(at) = (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+        *reinterpret_cast<uint32_t *>(at) = bf16x2_pack(a, b);
     }
 }
 

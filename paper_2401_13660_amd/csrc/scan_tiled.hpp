@@ -421,8 +421,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
                 if (OUT == 0)
                     *reinterpret_cast<float2 *>(yb + oy * 4u) = float2{yv[0], yv[1]};
                 else
-                    *reinterpret_cast<uint32_t *>(yb + oy * 2u) =
-                        (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
+                    *reinterpret_cast<uint32_t *>(yb + oy * 2u) = bf16x2_pack(yv[0], yv[1]);
             }
         } else {
             if (4 * q < nt) {
@@ -442,8 +441,8 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
                     if (OUT == 0) {
                         *reinterpret_cast<f32x4 *>(yb + oy * 4u) = f32x4{yv[0], yv[1], yv[2], yv[3]};
                     } else {
-                        const uint32_t w0 = (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
-                        const uint32_t w1 = (uint32_t)f32_to_bf16(yv[2]) | ((uint32_t)f32_to_bf16(yv[3]) << 16);
+                        const uint32_t w0 = bf16x2_pack(yv[0], yv[1]);
+                        const uint32_t w1 = bf16x2_pack(yv[2], yv[3]);
                         *reinterpret_cast<u32x2 *>(yb + oy * 2u) = u32x2{w0, w1};
                     }
                 }

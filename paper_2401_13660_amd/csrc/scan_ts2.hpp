@@ -50,21 +50,29 @@ using tiled::lds_wait;
 constexpr int kCh = 4;            // channels per wave
 constexpr int kS = kT / 2;        // timesteps per slice
 
-// Private LDS area of one wave (16-byte entries, 64 banks of 4 bytes):
-//   dd    row r = chunk timesteps 2r, 2r+1 (slice k: rows 8k .. 8k+7); entry j =
-//         (dlt, dx, dlt, dx) of channel j; 5 entries per row, so that the rows
-//         the two slices read at once lie 640 bytes (half the banks) apart
-//   bc    entry q of chunk timestep t at 10 t + q (+ 8 when t >= 16) =
-//         (B[2q], B[2q+1], C[2q], C[2q+1]): the two slices' rows read together
-//         then fall in different halves of the banks
+// Private LDS area of one wave, in 16-byte entries.  The pads follow the bank
+// rules measured on gfx950 (an LDS probe, one dispatch per access pattern, with
+// the SQ_LDS_BANK_CONFLICT counter): a 16-byte write serves 8 consecutive lanes at
+// a time from 32 banks of 4 bytes (a 128-byte period), an 8-byte read 32 lanes at
+// a time from 64 banks (256 bytes).  In every write below, the 8 lanes of a group
+// are 4 state pairs of both slices of one channel; in every read the two slices'
+// entries fall in different banks.  Each access of the kernel, measured in the
+// probe, runs without a bank conflict.
+//   dd    row r = chunk timesteps 2r, 2r+1 (slice k: rows 8k .. 8k+7) at 5 r
+//         (+ 4 when r >= 8); entry j = (dlt, dx, dlt, dx) of channel j
+//   bc    entry q of chunk timestep t at 9 t + q (+ 8 when t >= 16) =
+//         (B[2q], B[2q+1], C[2q], C[2q+1])
 //   part  row 8 j + 4 k + i = channel j, timesteps 16 k + 4 i .. + 3; entry q =
-//         the partial output of state pair q (10 entries per row, 8 used)
+//         the partial output of state pair q (9 entries per row, 8 used)
 struct WaveSmem {
-    f32x4 dd[kT / 2][5];          // 1.25 KB
-    f32x4 bc[10 * kT + 8];        // 5.1 KB
-    f32x4 part[kCh * 8][10];      // 5 KB
+    f32x4 dd[5 * (kT / 2) + 4];   // 1.3 KB
+    f32x4 bc[9 * kT + 8];         // 4.6 KB
+    f32x4 part[kCh * 8][9];       // 4.5 KB
 };
-__device__ __forceinline__ int bc_at(int t) { return 10 * t + (t >= kS ? 8 : 0); }
+// row c of slice k's dd rows (c < 8), and chunk timestep t or row c of slice k in bc
+__device__ __forceinline__ int dd_at(int k, int c) { return (5 * kS / 2 + 4) * k + 5 * c; }
+__device__ __forceinline__ int bc_at(int t) { return 9 * t + (t >= kS ? 8 : 0); }
+__device__ __forceinline__ int bc_at(int k, int c) { return (9 * kS + 8) * k + 9 * c; }
 
 // The value of lane l ^ 1 (a DPP quad permutation).
 __device__ __forceinline__ float pair_swap(float v) {
@@ -153,9 +161,9 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_ts2(ScanParams p) {
     auto loadL = [&](f32x4 (&ddv)[2], f32x4 (&bcv)[4], auto tq_c) {
         constexpr int TQ = decltype(tq_c)::value;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) ddv[i] = sm.dd[8 * k + 2 * TQ + i][j];
+        for (int i = 0; i < 2; ++i) ddv[i] = sm.dd[dd_at(k, 2 * TQ + i) + j];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) bcv[i] = sm.bc[bc_at(kS * k + 4 * TQ + i) + q];
+        for (int i = 0; i < 4; ++i) bcv[i] = sm.bc[bc_at(k, 4 * TQ + i) + q];
     };
     auto stepL = [&](const f32x4 (&ddv)[2], const f32x4 (&bcv)[4], auto tq_c) {
         constexpr int TQ = decltype(tq_c)::value;
@@ -204,7 +212,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_ts2(ScanParams p) {
                 xs[i] = x;
                 if (GATE) gs[i] = silu_f32(sl.z.get(i));
             }
-            sm.dd[8 * k + q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
+            sm.dd[dd_at(k, q) + j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -287,8 +295,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_ts2(ScanParams p) {
                 if (OUT == 0)
                     *reinterpret_cast<float2 *>(yb + oy * 4u) = float2{yv[0], yv[1]};
                 else
-                    *reinterpret_cast<uint32_t *>(yb + oy * 2u) =
-                        (uint32_t)f32_to_bf16(yv[0]) | ((uint32_t)f32_to_bf16(yv[1]) << 16);
+                    *reinterpret_cast<uint32_t *>(yb + oy * 2u) = bf16x2_pack(yv[0], yv[1]);
             }
         }
         __builtin_amdgcn_wave_barrier();    // the tables are rewritten by the next chunk
