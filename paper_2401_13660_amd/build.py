@@ -1,5 +1,6 @@
 """Build the HIP library libmbscan.so in-tree (gfx950 only), the issue-rate
-micro-benchmark behind the instruction cost model (csrc/issue_rates.hip), and
+micro-benchmark behind the instruction cost model (csrc/issue_rates.hip), the
+LDS bank probe behind the time-split kernel's tables (csrc/lds_banks.hip), and
 the exhaustive check of the bf16 pair conversion (csrc/bf16_pack_check.hip).
 
     python -m paper_2401_13660_amd.build
@@ -40,6 +41,7 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed to build libmbscan.so")
     os.replace(tmp, LIB)
     build_issue_rates(verbose)
+    build_lds_banks(verbose)
     build_bf16_pack_check(verbose)
     return LIB
 
@@ -63,6 +65,11 @@ def build_tool(name: str, verbose: bool = False) -> str:
 def build_issue_rates(verbose: bool = False) -> str:
     """The stand-alone issue-rate program (run it on the GPU: ./issue_rates)."""
     return build_tool("issue_rates", verbose)
+
+
+def build_lds_banks(verbose: bool = False) -> str:
+    """The LDS bank probe behind the time-split kernel's table layout (./lds_banks)."""
+    return build_tool("lds_banks", verbose)
 
 
 def build_bf16_pack_check(verbose: bool = False) -> str:
