@@ -116,9 +116,13 @@ template <int DT> __device__ __forceinline__ void store2(const char *base, uint3
 }
 
 // Private LDS area of one wave (13.75 KB); padded rows spread reads and writes
-// over the banks.
+// over the banks.  A 16-byte write serves 8 consecutive lanes (one channel) at a
+// time from 32 banks (a 128-byte period, measured); lane q writes timesteps 2q and
+// 2q + 1, so the dd rows are permuted (dd_row) to put those 8 writes in 8
+// different bank quads.
+__device__ __forceinline__ constexpr int dd_row(int t) { return (t >> 1) + (t & 1) * (kT / 2); }
 struct WaveSmem {
-    f32x4 dd[kT][kCh + 1];            // (dlt, dlt*u, ds, u) of timestep t, channel j
+    f32x4 dd[kT][kCh + 1];            // row dd_row(t): (dlt, dlt*u, ds, u) of timestep t, channel j
     f32x4 bc[kT][kQ + 2];             // (B[2q], B[2q+1], C[2q], C[2q+1]) of timestep t
     f32x4 pa[kCh * (kT / 4)][kQ + 1]; // per-state-pair partials, 4 timesteps per entry
     f32x4 pb[kCh * (kT / 4)][kQ + 1];
@@ -247,7 +251,7 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
         for (int k = 0; k < 2; ++k) {
             const float v = sl.dl.get(k) + bias;
             const float dl = SOFTPLUS ? softplus_f32(v) : v;
-            sm.dd[2 * q + k][j] = f32x4{dl, dl * sl.u.get(k), 0.0f, 0.0f};
+            sm.dd[dd_row(2 * q + k)][j] = f32x4{dl, dl * sl.u.get(k), 0.0f, 0.0f};
             sm.bc[2 * j + k][q] = f32x4{sl.b0.get(k), sl.b1.get(k), 0.0f, 0.0f};
         }
         issue(sl, t0 + 2 * kT);
@@ -260,7 +264,7 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
             float2 dvs[4], bvs[4];                      // (dlt, dlt*u), (B0, B1) of 4 steps, read together
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
-                dvs[k] = lo2(sm.dd[4 * tq + k][j]);
+                dvs[k] = lo2(sm.dd[dd_row(4 * tq + k)][j]);
                 bvs[k] = lo2(sm.bc[4 * tq + k][q]);
             }
 #pragma unroll
@@ -487,7 +491,7 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
             dlv[k] = dl;
             dsv[k] = ds;
             sum_dD = __builtin_fmaf(ds, x, sum_dD);
-            sm.dd[2 * q + k][j] = live ? f32x4{dl, dl * x, ds, x} : f32x4{dl, 0.0f, 0.0f, x};
+            sm.dd[dd_row(2 * q + k)][j] = live ? f32x4{dl, dl * x, ds, x} : f32x4{dl, 0.0f, 0.0f, x};
             sm.bc[2 * j + k][q] = f32x4{sl.b0.get(k), sl.b1.get(k), sl.c0.get(k), sl.c1.get(k)};
         }
         issue(sl, t0 - 2 * kT);                         // refill with the chunk two further back
@@ -502,7 +506,7 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
             f32x4 bvs[4];                               // (B0, B1, C0, C1); C only with a gate
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
-                dvs[k] = lo2(sm.dd[4 * tq + k][j]);
+                dvs[k] = lo2(sm.dd[dd_row(4 * tq + k)][j]);
                 if (GATE) {
                     bvs[k] = sm.bc[4 * tq + k][q];
                 } else {
@@ -554,7 +558,7 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
             f32x4 dvs[4], bvs[4];                       // the 4 steps' operands, read together
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
-                dvs[k] = sm.dd[4 * tq + k][j];
+                dvs[k] = sm.dd[dd_row(4 * tq + k)][j];
                 bvs[k] = sm.bc[4 * tq + k][q];
             }
 #pragma unroll

@@ -83,9 +83,13 @@ template <> struct Raw2<0> {
     __device__ __forceinline__ float get(int i) const { return i ? v.y : v.x; }
 };
 
-// Private LDS area of one wave.  Rows are padded so that both the writes and
-// the reads of every table touch distinct banks (16-byte entries, 64 banks):
-//   dd    row r = timesteps 2r, 2r+1; entry j = (dlt, dx, dlt, dx) of channel j
+// Private LDS area of one wave.  Rows are padded so that the reads of every
+// table touch distinct banks (16-byte entries, 64 banks), and the dd rows are
+// permuted (dd_row) so that its writes do too: a 16-byte write serves 8
+// consecutive lanes at a time from 32 banks (a 128-byte period, measured), and
+// the 8 lanes of one channel write timestep pairs 2q and 2q + 1; rows of 9
+// entries in natural order put those 8 writes in pairs on 4 bank quads.
+//   dd    row dd_row(r) = timesteps 2r, 2r+1; entry j = (dlt, dx, dlt, dx) of channel j
 //   bc    row t; entry q = (B[2q], B[2q+1], C[2q], C[2q+1]) at timestep t
 //   part  row 8 j + tq = channel j, timesteps 4 tq .. 4 tq + 3; entry q = the
 //         partial output of state pair q at those four timesteps
@@ -94,6 +98,12 @@ constexpr int kBcRow = 10;      // 8 used + 2 pad
 constexpr int kPartRow = 9;     // 8 used + 1 pad
 // SHORT: the tables of a sequence of one 16-timestep half chunk (the verify
 // shape), half the size, so that twice as many waves fit in a CU's LDS.
+// The dd row of timestep pair r: pairs 2q and 2q + 1 go to rows q and 8 + q, so
+// that the 8 lanes of a channel write 8 different bank quads.  (The 16-timestep
+// tables have 8 rows; lane q writes row q only.)
+template <bool SHORT> __device__ __forceinline__ constexpr int dd_row(int r) {
+    return SHORT ? r : (r >> 1) + (r & 1) * (kT / 4);
+}
 template <bool SHORT> struct WaveSmemT {
     static constexpr int kSteps = SHORT ? kT / 2 : kT;
     f32x4 dd[kSteps / 2][kDdRow];                    // 2.25 KB (SHORT: 1.1 KB)
@@ -107,7 +117,8 @@ static_assert(sizeof(WaveSmemT<true>) * kWavesPerGroup * 5 <= 160 * 1024,
 // The segment aggregate pass (scan_seg_agg) needs neither C nor the output
 // partials.  It stages B two timesteps per entry, and the smaller area lets more
 // waves share a CU:
-//   b2    row r = timesteps 2r, 2r+1; entry q = (B[2q], B[2q+1]) at 2r, then at 2r+1
+//   b2    row dd_row(r) = timesteps 2r, 2r+1; entry q = (B[2q], B[2q+1]) at 2r, then at 2r+1
+// (the dd rows are permuted as in the scan's tables)
 struct WaveSmemPre {
     static constexpr int kSteps = kT;
     f32x4 dd[kT / 2][kDdRow];                 // 2.25 KB
@@ -263,7 +274,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     auto load4 = [&](f32x4 (&ddv)[2], f32x4 (&bcv)[4], auto tq_c) {
         constexpr int TQ = decltype(tq_c)::value;
 #pragma unroll
-        for (int k = 0; k < 2; ++k) ddv[k] = sm.dd[2 * TQ + k][j];
+        for (int k = 0; k < 2; ++k) ddv[k] = sm.dd[dd_row<SHORT>(2 * TQ + k)][j];
 #pragma unroll
         for (int k = 0; k < 4; ++k) bcv[k] = sm.bc[4 * TQ + k][q];
     };
@@ -289,7 +300,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
             const int cnt = (int)(pk - t0) + 1;
             float g0 = r0, g1 = r1;
             for (int i = 0; i < cnt; ++i) {
-                const f32x4 dv = sm.dd[i >> 1][j];
+                const f32x4 dv = sm.dd[dd_row<SHORT>(i >> 1)][j];
                 const float dl = (i & 1) ? dv.z : dv.x;
                 const float dx = (i & 1) ? dv.w : dv.y;
                 const f32x4 bv = sm.bc[i][q];
@@ -334,8 +345,8 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
             if constexpr (SHORT) {
                 sm.dd[q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
             } else {
-                sm.dd[2 * q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
-                sm.dd[2 * q + 1][j] = f32x4{dl[2], dx[2], dl[3], dx[3]};
+                sm.dd[dd_row<false>(2 * q)][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
+                sm.dd[dd_row<false>(2 * q + 1)][j] = f32x4{dl[2], dx[2], dl[3], dx[3]};
             }
         }
 #pragma unroll
@@ -581,8 +592,8 @@ __global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t s
     auto load2 = [&](f32x4 (&dv)[2], f32x4 (&bv)[2], int tq) {
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
-            dv[k] = sm.dd[2 * tq + k][j];
-            bv[k] = sm.b2[2 * tq + k][q];
+            dv[k] = sm.dd[dd_row<false>(2 * tq + k)][j];
+            bv[k] = sm.b2[dd_row<false>(2 * tq + k)][q];
         }
     };
     auto wave_sync = [] {
@@ -602,10 +613,10 @@ __global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t s
         // pairwise within the quad, then across chunks and lanes: the rounding
         // of the segment's sum stays small
         dsum += (dl[0] + dl[1]) + (dl[2] + dl[3]);
-        sm.dd[2 * q][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
-        sm.dd[2 * q + 1][j] = f32x4{dl[2], dx[2], dl[3], dx[3]};
-        sm.b2[2 * q][j] = f32x4{sl.B0.get(0), sl.B1.get(0), sl.B0.get(1), sl.B1.get(1)};
-        sm.b2[2 * q + 1][j] = f32x4{sl.B0.get(2), sl.B1.get(2), sl.B0.get(3), sl.B1.get(3)};
+        sm.dd[dd_row<false>(2 * q)][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
+        sm.dd[dd_row<false>(2 * q + 1)][j] = f32x4{dl[2], dx[2], dl[3], dx[3]};
+        sm.b2[dd_row<false>(2 * q)][j] = f32x4{sl.B0.get(0), sl.B1.get(0), sl.B0.get(1), sl.B1.get(1)};
+        sm.b2[dd_row<false>(2 * q + 1)][j] = f32x4{sl.B0.get(2), sl.B1.get(2), sl.B0.get(3), sl.B1.get(3)};
         wave_sync();
         issue_loads(sl, k + 2);
         {
