@@ -97,7 +97,10 @@ constexpr int kDdRow = 9;       // 16-byte entries per row: 8 used + 1 pad
 constexpr int kBcRow = 10;      // 8 used + 2 pad
 constexpr int kPartRow = 9;     // 8 used + 1 pad
 // SHORT: the tables of a sequence of one 16-timestep half chunk (the verify
-// shape), half the size, so that twice as many waves fit in a CU's LDS.
+// shape), about a third the size, so that 7 workgroups fit in a CU's LDS instead
+// of 2.  Their B/C rows have no pad (every write and read of a row covers its 8
+// entries at once), and lanes q and q ^ 1 add their partial outputs in registers
+// before the write, so a partial row holds 4 sums (+ 1 pad entry).
 // The dd row of timestep pair r: pairs 2q and 2q + 1 go to rows q and 8 + q, so
 // that the 8 lanes of a channel write 8 different bank quads.  (The 16-timestep
 // tables have 8 rows; lane q writes row q only.)
@@ -106,14 +109,19 @@ template <bool SHORT> __device__ __forceinline__ constexpr int dd_row(int r) {
 }
 template <bool SHORT> struct WaveSmemT {
     static constexpr int kSteps = SHORT ? kT / 2 : kT;
+    static constexpr int kPartW = SHORT ? kQ / 2 + 1 : kPartRow;
     f32x4 dd[kSteps / 2][kDdRow];                    // 2.25 KB (SHORT: 1.1 KB)
-    f32x4 bc[kSteps][SHORT ? kDdRow : kBcRow];       // 5 KB (SHORT: 2.25 KB, one pad entry
-                                                     // per row, so that 5 workgroups fit in a CU)
-    f32x4 part[kCh * (kSteps / 4)][kPartRow];        // 9 KB (4.5 KB)
+    f32x4 bc[kSteps][SHORT ? kQ : kBcRow];           // 5 KB (SHORT: 2 KB)
+    f32x4 part[kCh * (kSteps / 4)][kPartW];          // 9 KB (SHORT: 2.5 KB)
 };
 using WaveSmem = WaveSmemT<false>;
-static_assert(sizeof(WaveSmemT<true>) * kWavesPerGroup * 5 <= 160 * 1024,
-              "five workgroups of the 16-timestep tables fit the 160 KB of a CU's LDS");
+static_assert(sizeof(WaveSmemT<true>) * kWavesPerGroup * 7 <= 160 * 1024,
+              "seven workgroups of the 16-timestep tables fit the 160 KB of a CU's LDS");
+
+// v + the value of lane l ^ 1 (a DPP quad permutation): the same sum in both lanes.
+__device__ __forceinline__ float add_lane_xor1(float v) {
+    return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xf, 0xf, false));
+}
 // The segment aggregate pass (scan_seg_agg) needs neither C nor the output
 // partials.  It stages B two timesteps per entry, and the smaller area lets more
 // waves share a CU:
@@ -190,27 +198,6 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     const int64_t L = p.seqlen;
     const int n0 = 2 * q;
 
-    const int64_t rows = p.batch * p.dim;
-    float a2[2], h[2];
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-        a2[s] = p.A[dcl * kN + n0 + s] * kLog2e;
-        h[s] = (nseg == 1 && p.h0) ? p.h0[row * kN + n0 + s] : 0.0f;
-    }
-    if (nseg > 1) {
-        // carry-in: the copy of h0 (plane nseg - 1), then the aggregates of the
-        // earlier segments; folding (1, h0) into the zero state gives h0 exactly
-        auto fold = [&](int64_t plane) {
-            const f32x4 ph = *reinterpret_cast<const f32x4 *>(carry + ((plane * rows + row) * kN + n0) * 2);
-            h[0] = __builtin_fmaf(ph.x, h[0], ph.y);
-            h[1] = __builtin_fmaf(ph.z, h[1], ph.w);
-        };
-        fold(nseg - 1);
-        for (int64_t s2 = 0; s2 < seg; ++s2) fold(s2);
-    }
-    const float dskip = p.Dskip ? p.Dskip[dcl] : 0.0f;
-    const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
-
     // Global addressing: wave-uniform 64-bit bases (the wave's first channel
     // row, or state row 0 of B and C, at the segment start) plus 32-bit lane
     // offsets in elements, so the loads use the scalar-base form.
@@ -252,6 +239,35 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         sl.C0.load(cb, ob);
         sl.C1.load(cb, ob + (uint32_t)L);
     };
+    // The activation loads of the first chunks go out before the per-row
+    // operands below, whose loads are conditional (null pointers are allowed):
+    // in the other order the compiler made the activation addresses wait for
+    // them, two memory round trips before the first chunk (a whole call of the
+    // 16-byte verify shape).
+    issue_loads(s0, 0);
+    if constexpr (!SHORT) issue_loads(s1, kT);
+
+    const int64_t rows = p.batch * p.dim;
+    float a2[2], h[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+        a2[s] = p.A[dcl * kN + n0 + s] * kLog2e;
+        h[s] = (nseg == 1 && p.h0) ? p.h0[row * kN + n0 + s] : 0.0f;
+    }
+    if (nseg > 1) {
+        // carry-in: the copy of h0 (plane nseg - 1), then the aggregates of the
+        // earlier segments; folding (1, h0) into the zero state gives h0 exactly
+        auto fold = [&](int64_t plane) {
+            const f32x4 ph = *reinterpret_cast<const f32x4 *>(carry + ((plane * rows + row) * kN + n0) * 2);
+            h[0] = __builtin_fmaf(ph.x, h[0], ph.y);
+            h[1] = __builtin_fmaf(ph.z, h[1], ph.w);
+        };
+        fold(nseg - 1);
+        for (int64_t s2 = 0; s2 < seg; ++s2) fold(s2);
+    }
+    const float dskip = p.Dskip ? p.Dskip[dcl] : 0.0f;
+    const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
+
 
     // Phase B step TQ: timesteps 4 TQ .. 4 TQ + 3, operands already in registers.
     auto recur4 = [&](const f32x4 (&ddv)[2], const f32x4 (&bcv)[4], auto tq_c) {
@@ -269,7 +285,14 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
             h[1] = __builtin_fmaf(a1, h[1], dx * b1);
             acc4[k] = __builtin_fmaf(bcv[k][3], h[1], bcv[k][2] * h[0]);
         }
-        sm.part[kPS * j + TQ][q] = f32x4{acc4[0], acc4[1], acc4[2], acc4[3]};
+        if constexpr (SHORT) {
+            // state pairs q and q ^ 1 summed; both lanes write the same entry
+#pragma unroll
+            for (int k = 0; k < 4; ++k) acc4[k] = add_lane_xor1(acc4[k]);
+            sm.part[kPS * j + TQ][q >> 1] = f32x4{acc4[0], acc4[1], acc4[2], acc4[3]};
+        } else {
+            sm.part[kPS * j + TQ][q] = f32x4{acc4[0], acc4[1], acc4[2], acc4[3]};
+        }
     };
     auto load4 = [&](f32x4 (&ddv)[2], f32x4 (&bcv)[4], auto tq_c) {
         constexpr int TQ = decltype(tq_c)::value;
@@ -410,13 +433,13 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         }
         wave_sync();
 
-        // ---- C: sum the 8 partials of channel j at timesteps 2q, 2q+1 ----------
+        // ---- C: sum the 4 partial sums of channel j at timesteps 2q, 2q+1 ------
         if constexpr (SHORT) {
             // the partials of timesteps 2q, 2q+1 are one half of entry (j, q >> 1)
             const float2 *src = reinterpret_cast<const float2 *>(&sm.part[kPS * j + (q >> 1)][0]) + (q & 1);
             float2 acc = src[0];
 #pragma unroll
-            for (int w = 1; w < kQ; ++w) {
+            for (int w = 1; w < kQ / 2; ++w) {
                 acc.x += src[2 * w].x;
                 acc.y += src[2 * w].y;
             }
@@ -463,11 +486,9 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         wave_sync();   // part / dd / bc are rewritten by the next chunk
     };
 
-    issue_loads(s0, 0);
     if constexpr (SHORT) {
         chunk(s0, t_begin);                         // the one half chunk
     } else {
-        issue_loads(s1, kT);
         int64_t t0 = t_begin;
         for (; t0 + 2 * kT <= t_end; t0 += 2 * kT) {   // pairs of full chunks
             chunk(s0, t0);
