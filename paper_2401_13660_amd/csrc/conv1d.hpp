@@ -56,6 +56,31 @@ template <> __device__ __forceinline__ void load8<0>(const void *base, int64_t o
     }
 }
 
+// The last H (1..3) activations of the span of 8 at element offset off, t[j] =
+// activation 8 - H + j.  Only the words that hold them are loaded: a loaded word
+// that is never used frees its register at once, and the compiler then waits
+// for the load to land before reusing it (a memory round trip per span).
+template <int DT, int H> __device__ __forceinline__ void load_tail(const void *base, int64_t off, float (&t)[H]) {
+    static_assert(H >= 1 && H <= 3, "kernel sizes 2..4");
+    if constexpr (DT == 1) {
+        const uint16_t *b = static_cast<const uint16_t *>(base) + off;
+        if constexpr (H == 3) {
+            const u32x2 r = *reinterpret_cast<const u32x2 *>(b + 4);      // activations 4..7
+            t[0] = bf16_hi(r[0]);
+            t[1] = bf16_lo(r[1]);
+            t[2] = bf16_hi(r[1]);
+        } else {
+            const uint32_t r = *reinterpret_cast<const uint32_t *>(b + 6);   // activations 6, 7
+            if constexpr (H == 2) t[0] = bf16_lo(r);
+            t[H - 1] = bf16_hi(r);
+        }
+    } else {
+        const float *f = static_cast<const float *>(base) + off + (kSpan - H);
+#pragma unroll
+        for (int j = 0; j < H; ++j) t[j] = f[j];
+    }
+}
+
 template <int DT> __device__ __forceinline__ void store8(void *base, int64_t off, const float (&v)[kSpan]);
 template <> __device__ __forceinline__ void store8<1>(void *base, int64_t off, const float (&v)[kSpan]) {
     u32x4 r;
@@ -88,47 +113,55 @@ __global__ __launch_bounds__(kThreads) void conv1d_fwd_vec(ConvParams p, uint32_
     const uint32_t first = (blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)) * (64 * kVecPerThread) +
                            (threadIdx.x & 63);
 
-    float cur[kVecPerThread][kSpan], prev[kVecPerThread][kSpan];
+    // Every load of the thread (its spans, the neighbouring spans' last inputs,
+    // the taps, bias and carried state of their rows) is issued before any of
+    // them is used: one memory round trip per thread.
+    float cur[kVecPerThread][kSpan], prev[kVecPerThread][H > 0 ? H : 1];
+    float w[kVecPerThread][K], bv[kVecPerThread], st[kVecPerThread][H > 0 ? H : 1];
+    uint32_t row[kVecPerThread], sp[kVecPerThread];
 #pragma unroll
     for (int v = 0; v < kVecPerThread; ++v) {
         // a span past the last one reads the last span again (never stored)
         const uint32_t g = first + v * 64 < total ? first + v * 64 : total - 1;
         load8<IN>(p.x, (int64_t)g * kSpan, cur[v]);
-        if (H > 0) load8<IN>(p.x, (int64_t)(g > 0 ? g - 1 : 0) * kSpan, prev[v]);
+        if constexpr (H > 0) load_tail<IN, H>(p.x, (int64_t)(g > 0 ? g - 1 : 0) * kSpan, prev[v]);
+    }
+#pragma unroll
+    for (int v = 0; v < kVecPerThread; ++v) {
+        const uint32_t g = first + v * 64 < total ? first + v * 64 : total - 1;
+        row[v] = g / nspan;
+        sp[v] = g - row[v] * nspan;
+        const uint32_t d = row[v] % (uint32_t)p.dim;
+#pragma unroll
+        for (int i = 0; i < K; ++i) w[v][i] = p.w[d * K + i];
+        bv[v] = p.bias ? p.bias[d] : 0.0f;
+#pragma unroll
+        for (int j = 0; j < H; ++j)
+            st[v][j] = (sp[v] == 0 && p.state_in) ? p.state_in[(int64_t)row[v] * H + j] : 0.0f;
     }
 
 #pragma unroll
     for (int v = 0; v < kVecPerThread; ++v) {
-        const uint32_t g = first + v * 64;
-        if (g >= total) break;
-        const uint32_t row = g / nspan;
-        const uint32_t sp = g - row * nspan;
-        const uint32_t d = row % (uint32_t)p.dim;
-        const int64_t base = (int64_t)row * L;
-        float w[K];
-#pragma unroll
-        for (int i = 0; i < K; ++i) w[i] = p.w[d * K + i];
-        const float b = p.bias ? p.bias[d] : 0.0f;
+        if (first + v * 64 >= total) break;
+        const int64_t base = (int64_t)row[v] * L;
         float xin[H + kSpan];
 #pragma unroll
         for (int i = 0; i < kSpan; ++i) xin[H + i] = cur[v][i];
 #pragma unroll
-        for (int j = 0; j < H; ++j)
-            xin[j] = sp > 0 ? prev[v][kSpan - H + j]
-                            : (p.state_in ? p.state_in[(int64_t)row * H + j] : 0.0f);
+        for (int j = 0; j < H; ++j) xin[j] = sp[v] > 0 ? prev[v][j] : st[v][j];
         float out[kSpan];
 #pragma unroll
         for (int i = 0; i < kSpan; ++i) {
-            float acc = b;
+            float acc = bv[v];
 #pragma unroll
-            for (int k = 0; k < K; ++k) acc = __builtin_fmaf(w[k], xin[i + k], acc);
+            for (int k = 0; k < K; ++k) acc = __builtin_fmaf(w[v][k], xin[i + k], acc);
             out[i] = p.apply_silu ? silu_f32(acc) : acc;
         }
-        store8<OUT>(p.y, base + (int64_t)sp * kSpan, out);
+        store8<OUT>(p.y, base + (int64_t)sp[v] * kSpan, out);
         // the span holding the last input writes the next state: inputs L-H .. L-1
-        if (H > 0 && p.state_out && sp == nspan - 1) {
+        if (H > 0 && p.state_out && sp[v] == nspan - 1) {
 #pragma unroll
-            for (int j = 0; j < H; ++j) p.state_out[(int64_t)row * H + j] = xin[kSpan + j];
+            for (int j = 0; j < H; ++j) p.state_out[(int64_t)row[v] * H + j] = xin[kSpan + j];
         }
     }
 }

@@ -27,23 +27,17 @@ __global__ __launch_bounds__(256) void scan_step_kernel(StepParams p) {
     const int64_t d = (int64_t)blockIdx.x * kStepRowsPerBlock<N> + tid / LANES;
     const bool dlive = d < p.dim;
     const int64_t dc = dlive ? d : 0;          // dead lanes still take part in the shuffles
-    // per channel: A, and the optional bias and skip (an absent one reads a
-    // stand-in of the same size, A, whose value is discarded)
-    float av[S];
-#pragma unroll
-    for (int s = 0; s < S; ++s) av[s] = p.A[dc * N + part * S + s] * kLog2e;
-    const float bias_raw = (p.dt_bias ? p.dt_bias : p.A)[dc];
-    const float dskip_raw = (p.Dskip ? p.Dskip : p.A)[dc];
-    const float bias = p.dt_bias ? bias_raw : 0.0f;
-    const float dskip = p.Dskip ? dskip_raw : 0.0f;
-
     for (int64_t b = blockIdx.y; b < p.batch; b += gridDim.y) {
         const int64_t r = b * p.dim + dc;
         // Every load is issued before the first use of any of them, so that a
-        // step costs one round trip to memory instead of three (activations, then
-        // state, then gate).  An absent gate reads u instead, discarded.  The
-        // lanes of a row read the same activation words.
-        float hs[S], bv[S], cv[S];
+        // step costs one round trip to memory instead of several (activations,
+        // state, gate and the per-channel operands).  The per-channel operands
+        // are loaded inside the loop, after the state, for that reason: loaded
+        // (and scaled) before it, the compiler waited for them before issuing
+        // the loop's loads.  An absent gate reads u instead, an absent bias or
+        // skip reads A, each discarded.  The lanes of a row read the same
+        // activation words.
+        float hs[S], bv[S], cv[S], ar[S];
 #pragma unroll
         for (int s = 0; s < S; ++s) {
             const int n = part * S + s;
@@ -54,13 +48,19 @@ __global__ __launch_bounds__(256) void scan_step_kernel(StepParams p) {
         const float x = Act<IN>::ld(p.u, r);
         const float draw = Act<IN>::ld(p.delta, r);
         const float z_raw = Act<IN>::ld(p.z ? p.z : p.u, r);
+#pragma unroll
+        for (int s = 0; s < S; ++s) ar[s] = p.A[dc * N + part * S + s];
+        const float bias_raw = (p.dt_bias ? p.dt_bias : p.A)[dc];
+        const float dskip_raw = (p.Dskip ? p.Dskip : p.A)[dc];
+        const float bias = p.dt_bias ? bias_raw : 0.0f;
+        const float dskip = p.Dskip ? dskip_raw : 0.0f;
         const float v = draw + bias;
         const float dlt = p.delta_softplus ? softplus_f32(v) : v;
         const float dx = dlt * x;
         float acc = 0.0f;
 #pragma unroll
         for (int s = 0; s < S; ++s) {
-            const float abar = hw_exp2(dlt * av[s]);
+            const float abar = hw_exp2(dlt * (ar[s] * kLog2e));
             hs[s] = __builtin_fmaf(abar, hs[s], dx * bv[s]);
             acc = __builtin_fmaf(cv[s], hs[s], acc);
         }
