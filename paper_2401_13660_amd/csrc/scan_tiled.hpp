@@ -173,20 +173,32 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
     // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2);
     // renumber them so that an XCD works on a contiguous range of (batch,
     // channel) groups and the B/C rows of a batch stay in one or two L2s.
-    const uint32_t per_xcd = gridDim.x / 8;
-    const uint32_t blk = blockIdx.x;
-    const uint32_t lwg = blk < per_xcd * 8 ? (blk % 8) * per_xcd + blk / 8 : blk;
-    const uint32_t wid = lwg * kWavesPerGroup + wave;
-    if (wid >= n_cg * (uint32_t)p.batch * nseg) return;   // whole wave leaves together
     // Time segment innermost: the waves resident together work on every segment.
     // Their loads then spread over the L2 sets even when the row stride is a
     // multiple of 128 KB (L = 65536), where the same timestep of every row falls
     // in the same sets: ordered by segment, the 1.6B layer's scan fetched 2.54 GB
     // for 1.81 GB of activations, in this order 1.99 GB.
-    const uint32_t rest = wid / nseg;
-    const int64_t seg = wid - rest * nseg;
-    const uint32_t bq = rest / n_cg;
-    const int64_t cg = rest - bq * n_cg;
+    // SHORT: a two-dimensional grid (channel groups x batch), so that a wave finds
+    // its group without a division (its B/C rows are too few for the XCD order
+    // to matter).
+    uint32_t seg32 = 0, bq, cg32;
+    if constexpr (SHORT) {
+        cg32 = blockIdx.x * kWavesPerGroup + wave;
+        bq = blockIdx.y;
+        if (cg32 >= n_cg) return;                    // whole wave leaves together
+    } else {
+        const uint32_t per_xcd = gridDim.x / 8;
+        const uint32_t blk = blockIdx.x;
+        const uint32_t lwg = blk < per_xcd * 8 ? (blk % 8) * per_xcd + blk / 8 : blk;
+        const uint32_t wid = lwg * kWavesPerGroup + wave;
+        if (wid >= n_cg * (uint32_t)p.batch * nseg) return;   // whole wave leaves together
+        const uint32_t rest = wid / nseg;
+        seg32 = wid - rest * nseg;
+        bq = rest / n_cg;
+        cg32 = rest - bq * n_cg;
+    }
+    const int64_t seg = seg32;
+    const int64_t cg = cg32;
     const int64_t b = bq;
     const int64_t t_begin = seg * seg_len;
     const int64_t t_end = t_begin + seg_len < p.seqlen ? t_begin + seg_len : p.seqlen;
@@ -771,7 +783,7 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream, float *lent) {
     const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;
     void *args[] = {&p, &seg_len, &carry};
     // One 16-timestep half chunk per wave (the verify shape): half-size tables.
-    const bool short_seq = p.seqlen == kT / 2 && nseg == 1 && !p.ck;
+    const bool short_seq = p.seqlen == kT / 2 && nseg == 1 && !p.ck && p.batch <= 65535;
     const void *main_fn =
         short_seq ? (p.npos > 0
                          ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, true, false, true>)
@@ -780,7 +792,9 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream, float *lent) {
         : p.ck       ? reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false, true>)
                      : reinterpret_cast<const void *>(&scan_fwd_tiled<IN, OUT, GATE, SP, false>);
     const size_t main_lds = short_seq ? sizeof(WaveSmemT<true>) * kWavesPerGroup : lds;
-    e = hipLaunchKernel(main_fn, dim3((unsigned)blocks), dim3(kThreads), args, main_lds, st);
+    const dim3 grid = short_seq ? dim3((unsigned)((n_cg + kWavesPerGroup - 1) / kWavesPerGroup), (unsigned)p.batch)
+                                : dim3((unsigned)blocks);
+    e = hipLaunchKernel(main_fn, grid, dim3(kThreads), args, main_lds, st);
     if (carry && !lent) {
         const hipError_t f = hipFreeAsync(carry, st);
         if (e == hipSuccess) e = f;
