@@ -63,6 +63,19 @@ def test_one_half_chunk(dtype, gated, softplus, out):
                          delta_softplus=softplus)
 
 
+# The 16-byte kernel runs on a two-dimensional grid (channel groups x batch), whose
+# second dimension holds at most 65535 batch elements; a larger batch takes the
+# full-table kernel.  Both sides of that limit, on sampled rows.
+@pytest.mark.parametrize("batch", [65535, 65536])
+def test_one_half_chunk_at_the_grid_limit(batch):
+    inp = make_inputs(batch, 8, 16, 16, dtype="bf16", seed=22, with_h0=True)
+    announce(f"L=16 ({batch}, 8) bf16")
+    y, h = gpu_fwd(inp)
+    rows = np.unique(np.concatenate([np.arange(0, 64), np.arange(batch * 8 - 64, batch * 8),
+                                     np.random.default_rng(5).integers(0, batch * 8, 128)]))
+    check_against_oracle(inp, y, h, rows=rows)
+
+
 def test_dskip_zero_isolates_ssm_term():
     inp = make_inputs(2, 192, 2048, 16, dtype="bf16", seed=3, with_D=False)
     announce("Dskip = 0 (2, 192, 2048)")
