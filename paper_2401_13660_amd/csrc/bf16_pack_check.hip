@@ -69,7 +69,7 @@ int main() {
         }
     }
     std::printf("bf16 pair conversion: %llu of %llu results differ\n", total, 2ull << 32);
-    hipFree(d_bad);
-    hipFree(d_first);
+    (void)hipFree(d_bad);
+    (void)hipFree(d_first);
     return total == 0 ? 0 : 1;
 }

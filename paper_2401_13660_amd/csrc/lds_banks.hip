@@ -180,8 +180,8 @@ int main() {
         if (!run(pats[i], &c)) return 2;
         std::printf("| %zu | %s | %.2f |\n", i + 1, pats[i].name.c_str(), c);
     }
-    hipFree(d_a);
-    hipFree(d_out);
-    hipFree(d_clk);
+    (void)hipFree(d_a);
+    (void)hipFree(d_out);
+    (void)hipFree(d_clk);
     return 0;
 }
