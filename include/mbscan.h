@@ -114,12 +114,13 @@ int mb_scan_fwd(const mb_scan_desc *desc,
  * those of mb_scan_fwd; the call itself allocates nothing.
  *
  * Where mb_scan_fwd cuts a sequence into time segments (few rows, long
- * sequences) it allocates a carry buffer of nseg x batch x dim x 128 bytes on
- * the stream.  This entry point keeps that carry in a static device array of
+ * sequences) it allocates a carry buffer on the stream: one plane of
+ * batch x dim x 128 bytes per pre-pass piece (1 or 2 per segment but the last)
+ * and one for h0.  This entry point keeps that carry in a static device array of
  * 8 MiB instead: each GPU the library runs on holds its own copy until the
  * process ends.  A problem whose carry would exceed it returns MB_ERR_SHAPE
- * (on a 256-CU MI355X the forward's segment choice never needs more than
- * 4 MiB).  The array keeps the last call's contents; nothing in it needs to
+ * (on a 256-CU MI355X the forward's segment choice stays below 8 MiB: 7.3 MiB
+ * for batch 1, dim 4608, L 65536).  The array keeps the last call's contents; nothing in it needs to
  * start at zero (the segment pre-pass writes every carry entry before the scan
  * reads it).  Every call on one GPU shares that GPU's array, so calls that may
  * overlap in time on one GPU (other streams, other threads) race: serialise

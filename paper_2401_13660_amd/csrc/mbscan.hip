@@ -230,9 +230,9 @@ hipError_t bwd_launch(mbs::bwd::BwdParams &p, bool have_ck, float *dA, float *dB
         f.u = p.u; f.delta = p.delta; f.Bm = p.Bm; f.Cm = p.Cm;
         f.A = p.A; f.dt_bias = p.dt_bias;
         f.delta_softplus = p.delta_softplus;
-        int64_t seg_len = p.ck_seg_len;
+        int64_t seg_len = p.ck_seg_len, npieces = ck_nseg - 1;   // one piece per segment
         float *fagg = const_cast<float *>(p.fagg);
-        void *fargs[] = {&f, &seg_len, &fagg};
+        void *fargs[] = {&f, &seg_len, &npieces, &fagg};
         namespace T = mbs::tiled;
         const dim3 grid_pre((unsigned)((waves * (ck_nseg - 1) + T::kWavesPerGroup - 1) / T::kWavesPerGroup));
         e = hipLaunchKernel(reinterpret_cast<const void *>(&T::scan_seg_agg<IN, SP>), grid_pre, dim3(T::kThreads),
@@ -440,8 +440,9 @@ int scan_fwd_impl(const mb_scan_desc *desc, const void *u, const void *delta, co
     float *lent = nullptr;
     if (no_alloc && tiled_ok(p, N, desc->in_dtype, desc->out_dtype)) {
         // the segment carry lives in this device's copy of the static scratch array
-        int64_t seg_len;
-        const size_t need = mbs::tiled::fwd_carry_bytes(p, mbs::tiled::fwd_segments(p, &seg_len));
+        int64_t seg_len, pieces;
+        const int64_t nseg = mbs::tiled::fwd_segments(p, &seg_len, &pieces);
+        const size_t need = mbs::tiled::fwd_carry_bytes(p, nseg, pieces);
         if (need > kScratchBytes) return MB_ERR_SHAPE;
         if (need > 0) {
             const int st = scratch_for_current_device(reinterpret_cast<void **>(&lent));

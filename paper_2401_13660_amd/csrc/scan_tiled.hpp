@@ -133,9 +133,11 @@ struct WaveSmemPre {
     f32x4 b2[kT / 2][kDdRow];                 // 2.25 KB
 };
 
-// The scan.  With several time segments, the wave of segment s starts from the
-//   copy of h0 that scan_seg_agg leaves in carry plane nseg - 1, folded with the
-//   aggregates of segments 0..s-1 (carry planes 0..s-1).  It never reads h0
+// The scan.  With several time segments, each cut into `pieces` equal pieces for
+//   the pre-pass, the wave of segment s starts from the copy of h0 that
+//   scan_seg_agg leaves in carry plane pieces (nseg - 1), folded with the
+//   aggregates of pieces 0 .. pieces s - 1 (carry planes 0 .. pieces s - 1), those
+//   of the segments before it in time order.  It never reads h0
 //   itself: the wave of the last segment may then write h_last over h0 while the
 //   waves of earlier segments of the same rows have not started (workgroups are
 //   not ordered).
@@ -155,7 +157,8 @@ template <int N> __device__ __forceinline__ void lds_wait() {
 }
 
 template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool POS, bool CK = false, bool SHORT = false>
-__global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len, const float *carry) {
+__global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t seg_len, int64_t pieces,
+                                                      const float *carry) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     using Smem = WaveSmemT<SHORT>;
@@ -267,15 +270,15 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
         h[s] = (nseg == 1 && p.h0) ? p.h0[row * kN + n0 + s] : 0.0f;
     }
     if (nseg > 1) {
-        // carry-in: the copy of h0 (plane nseg - 1), then the aggregates of the
-        // earlier segments; folding (1, h0) into the zero state gives h0 exactly
+        // carry-in: the copy of h0, then the aggregates of the earlier segments'
+        // pieces; folding (1, h0) into the zero state gives h0 exactly
         auto fold = [&](int64_t plane) {
             const f32x4 ph = *reinterpret_cast<const f32x4 *>(carry + ((plane * rows + row) * kN + n0) * 2);
             h[0] = __builtin_fmaf(ph.x, h[0], ph.y);
             h[1] = __builtin_fmaf(ph.z, h[1], ph.w);
         };
-        fold(nseg - 1);
-        for (int64_t s2 = 0; s2 < seg; ++s2) fold(s2);
+        fold(pieces * (nseg - 1));
+        for (int64_t s2 = 0; s2 < pieces * seg; ++s2) fold(s2);
     }
     const float dskip = p.Dskip ? p.Dskip[dcl] : 0.0f;
     const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
@@ -518,17 +521,23 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
 
 // ---- segment aggregates ------------------------------------------------------
 //
-// For every time segment but the last (seg_len timesteps, a multiple of 32) and
-// every state n of a row, the segment's element of the associative operator of
+// The scan's segments but the last are cut into pieces of piece_len timesteps
+// (a multiple of 32), npieces in all.  For every piece and every state n of a
+// row, the piece's element of the associative operator of
 // Section 2 ("Implementation"):
 //   P[n] = prod_t abar_t[n] = 2^(A[n] log2 e sum_t dlt_t),
 //   H[n] = sum_t (prod_{r > t} abar_r[n]) dlt_t B_t[n] x_t,
-// so that the state at the segment's end is P h_start + H.  H is the state the
-// recurrence reaches from a zero state at the segment's start; P is one
-// exponential of the segment's summed dlt, not a product of hundreds of
+// so that the state at the piece's end is P h_start + H.  H is the state the
+// recurrence reaches from a zero state at the piece's start; P is one
+// exponential of the piece's summed dlt, not a product of hundreds of
 // hardware exponentials near 1, whose rounding would drift and be carried into
 // every later segment by the fold P h + H.  The pairs (P, H) go to
-// carry[((seg * rows + row) * 16 + n) * 2 + {0, 1}].
+// carry[((piece * rows + row) * 16 + n) * 2 + {0, 1}].
+//
+// Pieces smaller than the scan's segments balance the pass: one wave per piece
+// and 8 channels, and with one piece per segment the 1.6B layer's 3,456 waves
+// leave 4 on some SIMDs and 3 on others, while 6,912 half-length pieces make 6.75
+// per SIMD against at most 7.
 //
 // A walk from the segment's end that stops once the running product of abar is
 // exactly zero in fp32 gives the same (P, H) with fewer timesteps, but with the
@@ -536,14 +545,15 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_tiled(ScanParams p, int64_t
 // every 8-channel wave decays too slowly for that within a segment, and the walk
 // costs a multiply more per step: measured slower on the 1.6B layer.
 //
-// The waves of segment 0 also copy h0 (or zeros) into plane nseg - 1 as the pairs
+// The waves of piece 0 also copy h0 (or zeros) into plane npieces as the pairs
 // (1, h0[n]), which the scan folds first.
 //
 // Lane l = 8 j + q as in the scan: channel j, states 2q and 2q+1.  Per chunk,
 // lane (j, q) forms dlt and dx of channel j at timesteps 4q .. 4q+3 and stages B
 // rows 2j and 2j+1 at those timesteps (the dd and b2 tables of WaveSmemPre).
 template <int IN, bool SOFTPLUS>
-__global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t seg_len, float *carry) {
+__global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t piece_len, int64_t npieces,
+                                                    float *carry) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     WaveSmemPre &sm = reinterpret_cast<WaveSmemPre *>(smem_raw)[wave];
@@ -552,19 +562,18 @@ __global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t s
     const int j = lane >> 3;
     const int q = lane & 7;
     const uint32_t n_cg = (uint32_t)((p.dim + kCh - 1) / kCh);
-    const uint32_t nseg = ((uint32_t)p.seqlen + (uint32_t)seg_len - 1) / (uint32_t)seg_len;
-    const uint32_t nsg = nseg - 1;                      // the segments that have an aggregate
+    const uint32_t nsg = (uint32_t)npieces;             // the pieces that have an aggregate
     const uint32_t per_xcd = gridDim.x / 8;
     const uint32_t blk = blockIdx.x;
     const uint32_t lwg = blk < per_xcd * 8 ? (blk % 8) * per_xcd + blk / 8 : blk;
     const uint32_t wid = lwg * kWavesPerGroup + wave;
     if (wid >= n_cg * (uint32_t)p.batch * nsg) return;   // whole wave leaves together
     const uint32_t rest = wid / nsg;
-    const int64_t seg = wid - rest * nsg;
+    const int64_t piece = wid - rest * nsg;
     const uint32_t bq = rest / n_cg;
     const int64_t cg = rest - bq * n_cg;
     const int64_t b = bq;
-    const int64_t t_begin = seg * seg_len;
+    const int64_t t_begin = piece * piece_len;
 
     const int64_t d = cg * kCh + j;
     const bool live = d < p.dim;
@@ -575,10 +584,10 @@ __global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t s
     const int64_t rows = p.batch * p.dim;
 
     float a2[2], h[2] = {0.0f, 0.0f};
-    float dsum = 0.0f;      // this lane's share of the segment's sum of dlt
+    float dsum = 0.0f;      // this lane's share of the piece's sum of dlt
 #pragma unroll
     for (int s = 0; s < 2; ++s) a2[s] = p.A[dcl * kN + n0 + s] * kLog2e;
-    if (seg == 0 && live) {
+    if (piece == 0 && live) {
         const float g0 = p.h0 ? p.h0[row * kN + n0] : 0.0f;
         const float g1 = p.h0 ? p.h0[row * kN + n0 + 1] : 0.0f;
         *reinterpret_cast<f32x4 *>(carry + (((int64_t)nsg * rows + row) * kN + n0) * 2) =
@@ -594,11 +603,11 @@ __global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t s
     const char *bb = static_cast<const char *>(p.Bm) + (b * kN * L + t_begin) * kEl;
     const uint32_t act_row = (uint32_t)((dcl - cg * kCh) * L);       // lane's channel row
     const uint32_t bc_row = (uint32_t)(2 * j * L);                   // B rows 2j, 2j+1
-    const uint32_t nch = (uint32_t)(seg_len / kT);
+    const uint32_t nch = (uint32_t)(piece_len / kT);
 
     struct Slot { Raw4<IN> u, dl, B0, B1; };
     Slot s0, s1;
-    // Chunk k starts at 32 k; past the segment's end the loads read the last
+    // Chunk k starts at 32 k; past the piece's end the loads read the last
     // chunk again (never consumed).
     auto issue_loads = [&](Slot &sl, uint32_t k) {
         const uint32_t tr = (k < nch ? k : nch - 1) * kT + 4 * q;
@@ -644,7 +653,7 @@ __global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t s
             dx[i] = dl[i] * sl.u.get(i);
         }
         // pairwise within the quad, then across chunks and lanes: the rounding
-        // of the segment's sum stays small
+        // of the piece's sum stays small
         dsum += (dl[0] + dl[1]) + (dl[2] + dl[3]);
         sm.dd[dd_row<false>(2 * q)][j] = f32x4{dl[0], dx[0], dl[1], dx[1]};
         sm.dd[dd_row<false>(2 * q + 1)][j] = f32x4{dl[2], dx[2], dl[3], dx[3]};
@@ -691,13 +700,13 @@ __global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t s
     }
     if (k < nch) chunk(s0, k);                      // an odd chunk count leaves one
     // the eight lanes of channel j hold its timesteps 4q .. 4q+3 of every chunk:
-    // after the butterfly each holds the whole segment's sum
+    // after the butterfly each holds the whole piece's sum
     dsum += __shfl_xor(dsum, 1);
     dsum += __shfl_xor(dsum, 2);
     dsum += __shfl_xor(dsum, 4);
     if (live) {
         const float P0 = hw_exp2(a2[0] * dsum), P1 = hw_exp2(a2[1] * dsum);
-        *reinterpret_cast<f32x4 *>(carry + ((seg * rows + row) * kN + n0) * 2) = f32x4{P0, h[0], P1, h[1]};
+        *reinterpret_cast<f32x4 *>(carry + ((piece * rows + row) * kN + n0) * 2) = f32x4{P0, h[0], P1, h[1]};
     }
 }
 
@@ -713,15 +722,27 @@ __global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t s
 // largest that fills the chip at most twice over: a third round, partly
 // filled, costs more than its shorter segments return.  Above the threshold
 // the pre-pass costs more than the extra occupancy returns.
-inline int64_t choose_segments(int64_t waves_base, int64_t L, int64_t resident, int64_t *seg_len) {
+// The pre-pass cuts each segment into `pieces` (1 or 2) equal pieces, one wave
+// per piece and 8 channels.  A SIMD takes as long as its largest number of
+// waves times the piece length, so 2 pieces are taken where that is shorter:
+// ceil(2 w / simds) / 2 below ceil(w / simds), for the w waves of whole
+// segments.  All its waves are resident at once (seven per SIMD).
+inline int64_t choose_segments(int64_t waves_base, int64_t L, int64_t resident, int64_t simds, int64_t *seg_len,
+                               int64_t *pieces) {
     int64_t nseg = 1;
     if (waves_base > 0 && waves_base * 8 < resident * 3) nseg = 2 * resident / waves_base;
     const int64_t max_seg = L / 256;
     if (nseg > max_seg) nseg = max_seg;
     if (nseg < 1) nseg = 1;
+    int64_t m = 1;
+    if (nseg > 1) {
+        const int64_t w = waves_base * (nseg - 1);
+        if ((2 * w + simds - 1) / simds < 2 * ((w + simds - 1) / simds)) m = 2;
+    }
     int64_t len = (L + nseg - 1) / nseg;
-    len = (len + 31) / 32 * 32;
+    len = (len + 32 * m - 1) / (32 * m) * (32 * m);     // pieces of a multiple of 32 timesteps
     *seg_len = len;
+    *pieces = m;
     return (L + len - 1) / len;
 }
 
@@ -738,17 +759,21 @@ inline int64_t device_cus() {
 // 4 waves per CU).
 inline int64_t resident_waves() { return 2 * kWavesPerGroup * device_cus(); }
 
-// The time segments the forward takes for p (1: none), and their length.
-inline int64_t fwd_segments(const ScanParams &p, int64_t *seg_len) {
+// The time segments the forward takes for p (1: none), their length and the
+// pre-pass pieces per segment.
+inline int64_t fwd_segments(const ScanParams &p, int64_t *seg_len, int64_t *pieces) {
     const int64_t n_cg = (p.dim + kCh - 1) / kCh;
     *seg_len = p.seqlen;
-    return p.seqlen >= 512 ? choose_segments(n_cg * p.batch, p.seqlen, resident_waves(), seg_len) : 1;
+    *pieces = 1;
+    return p.seqlen >= 512
+               ? choose_segments(n_cg * p.batch, p.seqlen, resident_waves(), 4 * device_cus(), seg_len, pieces)
+               : 1;
 }
 
-// Device bytes of the segment carry: the aggregates of segments 0 .. nseg-2,
-// then the copy of h0 (rows x 16 states x 2 floats per plane).
-inline size_t fwd_carry_bytes(const ScanParams &p, int64_t nseg) {
-    return nseg > 1 ? (size_t)nseg * (size_t)(p.batch * p.dim) * kN * 2 * sizeof(float) : 0;
+// Device bytes of the segment carry: the aggregates of the pieces of segments
+// 0 .. nseg-2, then the copy of h0 (rows x 16 states x 2 floats per plane).
+inline size_t fwd_carry_bytes(const ScanParams &p, int64_t nseg, int64_t pieces) {
+    return nseg > 1 ? (size_t)(pieces * (nseg - 1) + 1) * (size_t)(p.batch * p.dim) * kN * 2 * sizeof(float) : 0;
 }
 
 // lent: device memory of at least fwd_carry_bytes() for the carry, or null for
@@ -757,8 +782,8 @@ template <int IN, int OUT, bool GATE, bool SP>
 hipError_t fwd_tiled_sp(ScanParams &p, void *stream, float *lent) {
     hipStream_t st = static_cast<hipStream_t>(stream);
     const int64_t n_cg = (p.dim + kCh - 1) / kCh;
-    int64_t seg_len = p.seqlen;
-    const int64_t nseg = fwd_segments(p, &seg_len);
+    int64_t seg_len = p.seqlen, pieces = 1;
+    const int64_t nseg = fwd_segments(p, &seg_len, &pieces);
     float *carry = nullptr;
     const size_t lds = sizeof(WaveSmem) * kWavesPerGroup;
     hipError_t e;
@@ -766,12 +791,13 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream, float *lent) {
         if (lent) {
             carry = lent;
         } else {
-            e = hipMallocAsync(reinterpret_cast<void **>(&carry), fwd_carry_bytes(p, nseg), st);
+            e = hipMallocAsync(reinterpret_cast<void **>(&carry), fwd_carry_bytes(p, nseg, pieces), st);
             if (e != hipSuccess) return e;
         }
-        const int64_t waves = n_cg * p.batch * (nseg - 1);
+        int64_t piece_len = seg_len / pieces, npieces = pieces * (nseg - 1);
+        const int64_t waves = n_cg * p.batch * npieces;
         const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;
-        void *args[] = {&p, &seg_len, &carry};
+        void *args[] = {&p, &piece_len, &npieces, &carry};
         e = hipLaunchKernel(reinterpret_cast<const void *>(&scan_seg_agg<IN, SP>), dim3((unsigned)blocks),
                             dim3(kThreads), args, sizeof(WaveSmemPre) * kWavesPerGroup, st);
         if (e != hipSuccess) {
@@ -781,7 +807,7 @@ hipError_t fwd_tiled_sp(ScanParams &p, void *stream, float *lent) {
     }
     const int64_t waves = n_cg * p.batch * nseg;
     const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;
-    void *args[] = {&p, &seg_len, &carry};
+    void *args[] = {&p, &seg_len, &pieces, &carry};
     // One 16-timestep half chunk per wave (the verify shape): half-size tables.
     const bool short_seq = p.seqlen == kT / 2 && nseg == 1 && !p.ck && p.batch <= 65535;
     const void *main_fn =

@@ -328,8 +328,8 @@ namespace ts2 {
 // SIMDs (where the plain kernel would leave every SIMD with one wave at most).
 inline bool takes(const ScanParams &p) {
     if (p.npos > 0 || p.ck || p.seqlen < kT) return false;
-    int64_t seg_len;
-    if (tiled::fwd_segments(p, &seg_len) != 1) return false;
+    int64_t seg_len, pieces;
+    if (tiled::fwd_segments(p, &seg_len, &pieces) != 1) return false;
     const int64_t plain_waves = (p.dim + tiled::kCh - 1) / tiled::kCh * p.batch;
     return plain_waves <= 4 * tiled::device_cus();
 }
