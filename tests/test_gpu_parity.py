@@ -152,7 +152,7 @@ def test_h_last_may_alias_h0(L):
 
 # Shapes with few rows cut the sequence into time segments (a pre-pass of segment
 # aggregates, then one wave per segment): (1, 64, 4096) takes 16 segments,
-# (1, 61, 4112) 15 with dead lanes.  The waves of the last segment write h_last
+# (1, 61, 4112) 13 with dead lanes.  The waves of the last segment write h_last
 # while waves of earlier segments of the same rows may not have started, so the
 # scan must not read h0 itself there.  Each entry point that writes h_last is run
 # with h_last on top of h0.
@@ -244,11 +244,15 @@ def test_deterministic():
     assert torch.equal(y1, y2) and torch.equal(h1, h2)
 
 
-@pytest.mark.parametrize("shape", [(1, 64, 4096), (1, 61, 4112), (2, 24, 8192), (1, 8, 640)])
+# (1, 5996, 1296): 750 eight-channel waves (4 dead lanes), 5 segments of 288 bytes
+# (the last 144), and the pre-pass in one piece per segment (3,000 waves: 6 per
+# SIMD either way); the other shapes take two pieces per segment.
+@pytest.mark.parametrize("shape", [(1, 64, 4096), (1, 61, 4112), (2, 24, 8192), (1, 8, 640), (1, 5996, 1296)])
 @pytest.mark.parametrize("gated", [True, False])
 def test_time_segments(shape, gated):
     """Few (batch, channel) rows and a long sequence: the tiled path cuts time into
-    segments, a pre-pass computes each segment's aggregate and the scan folds them."""
+    segments, a pre-pass computes each segment's aggregate (in one or two pieces per
+    segment) and the scan folds them."""
     nb, dim, L = shape
     inp = make_inputs(nb, dim, L, 16, dtype="bf16", seed=15, with_h0=True, gated=gated, A_kind="random")
     announce(f"time segments {shape} gated={gated}")

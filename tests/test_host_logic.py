@@ -68,6 +68,8 @@ HAND = [
     ((767, 8192, 2048, 1024), (5, 1664, 1)),    # just below 3/8 of the resident waves; 3068 waves:
                                                 # ceil(5.99) = 6 = 2 ceil(2.996), so one piece
     ((768, 8192, 2048, 1024), (1, 8192, 1)),    # at 3/8: no segments
+    ((750, 1296, 2048, 1024), (5, 288, 1)),     # 4096 // 750 = 5 = 1296 // 256; 3000 waves: ceil(5.86)
+                                                # = 6 = 2 ceil(2.93), one piece; ceil(1296/5) = 260 -> 288
     ((576, 65536, 512, 256), (1, 65536, 1)),    # a device with 64 CUs: 576 waves fill it
     ((1, 16, 2048, 1024), (1, 32, 1)),          # one segment, its length rounded up to 32 (the launcher
                                                 # does not cut sequences below 512 bytes at all)

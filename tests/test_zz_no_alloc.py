@@ -14,7 +14,7 @@ pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not has_gpu(), reason="needs a
 def _both(inp):
     import paper_2401_13660_amd as mb
     t = to_device(inp)
-    kw = dict(D=t["Dskip"], dt_bias=t["dt_bias"], z=t["z"], h0=t["h0"])
+    kw = dict(D=t.get("Dskip"), dt_bias=t.get("dt_bias"), z=t.get("z"), h0=t.get("h0"))
     y_ref, h_ref = mb.scan_fwd(t["u"], t["delta"], t["A"], t["B"], t["C"], return_last_state=True, **kw)
     y = torch.full_like(y_ref, float("nan"))
     h = torch.full_like(h_ref, float("nan"))
@@ -48,3 +48,18 @@ def test_noalloc_h_last_on_h0():
                         z=t["z"], h0=state, out=y, h_last=state)
     torch.cuda.synchronize()
     check_against_oracle(inp, y, state)
+
+
+def test_noalloc_at_the_largest_carry():
+    """The 1.6B layer, (1, 4608, 65536): 7 segments whose pre-pass runs in 2 pieces
+    each, so the carry fills 13 planes of 4608 x 128 bytes (7.3 MiB of the 8 MiB
+    array).  Every output bit equals mb_scan_fwd's, whose rows are held to the fp64
+    oracle at this size by the full-size tests."""
+    from paper_2401_13660_amd.inputs import workload
+    inp = workload("mambabyte1p6b_L65536")
+    announce("mb_scan_fwd_noalloc at (1, 4608, 65536), 7.3 MiB of carry")
+    y_ref, h_ref, y, h = _both(inp)
+    assert torch.equal(y, y_ref), "y differs from mb_scan_fwd at (1, 4608, 65536)"
+    assert torch.equal(h, h_ref), "h_last differs from mb_scan_fwd at (1, 4608, 65536)"
+    rows = np.array([0, 1, 7, 8, 2303, 4599, 4607])
+    check_against_oracle(inp, y, h, rows=rows)
