@@ -726,7 +726,8 @@ __global__ __launch_bounds__(kThreads) void scan_seg_agg(ScanParams p, int64_t p
 // per piece and 8 channels.  A SIMD takes as long as its largest number of
 // waves times the piece length, so 2 pieces are taken where that is shorter:
 // ceil(2 w / simds) / 2 below ceil(w / simds), for the w waves of whole
-// segments.  All its waves are resident at once (seven per SIMD).
+// segments.  That takes 2 pieces only up to 7 waves per SIMD, as many as fit
+// with bf16 inputs (70 VGPRs), so those waves are all resident at once.
 inline int64_t choose_segments(int64_t waves_base, int64_t L, int64_t resident, int64_t simds, int64_t *seg_len,
                                int64_t *pieces) {
     int64_t nseg = 1;
