@@ -259,6 +259,16 @@ def test_time_segments(shape, gated):
     run_case(inp)
 
 
+def test_time_segments_f32_two_rounds():
+    """fp32 inputs at the 1.6B layer's width, (1, 4608, 2048): 7 segments of 320 bytes
+    (the last 128), the pre-pass in 2 pieces of 160 per segment.  Its 6,912 waves are
+    more than the 5 per SIMD that fit with fp32 inputs (83 VGPRs), so it runs in two
+    rounds."""
+    inp = make_inputs(1, 4608, 2048, 16, dtype="f32", seed=17, with_h0=True, A_kind="random")
+    announce("time segments fp32 (1, 4608, 2048), pre-pass in two rounds")
+    run_case(inp)
+
+
 def test_time_segments_deterministic():
     inp = make_inputs(1, 64, 4096, 16, dtype="bf16", seed=16, with_h0=True)
     announce("time segments determinism (1, 64, 4096)")
