@@ -193,8 +193,12 @@ int64_t bwd_partial_groups(int64_t batch, int64_t dim, int64_t nseg) {
 // share a SIMD; with at most half that many 8-channel waves the sequence is cut
 // into the most segments that fill the chip once, each at least 256 bytes and a
 // multiple of 32.  The aggregate pre-pass costs about a quarter of the backward's
-// work per timestep, well below what the extra waves return.
-int64_t bwd_segments(int64_t batch, int64_t dim, int64_t L, int64_t *seg_len) {
+// work per timestep, well below what the extra waves return.  The pre-pass cuts
+// each segment into `pieces` (1, 2 or 4), the most that keep its waves at 4 per
+// SIMD or fewer: one wave alone on a SIMD waits on its chain of dependent
+// operations, and up to 4 interleave.  Segments are then a multiple of 16 x pieces
+// timesteps (and of 32).
+int64_t bwd_segments(int64_t batch, int64_t dim, int64_t L, int64_t *seg_len, int64_t *pieces) {
     namespace W = mbs::bwd;
     const int64_t waves = (dim + W::kCh - 1) / W::kCh * batch;
     int64_t nseg = 1;
@@ -204,9 +208,16 @@ int64_t bwd_segments(int64_t batch, int64_t dim, int64_t L, int64_t *seg_len) {
         if (nseg > L / 256) nseg = L / 256;
         if (nseg < 1) nseg = 1;
     }
+    int64_t m = 1;
+    if (nseg > 1) {
+        const int64_t simds = 4 * mbs::tiled::device_cus();
+        while (m < 4 && 2 * m * waves * (nseg - 1) <= 4 * simds) m *= 2;
+    }
+    const int64_t unit = 16 * m > 32 ? 16 * m : 32;
     int64_t len = (L + nseg - 1) / nseg;
-    len = (len + 31) / 32 * 32;
+    len = (len + unit - 1) / unit * unit;
     *seg_len = len;
+    *pieces = m;
     return (L + len - 1) / len;
 }
 
@@ -245,7 +256,7 @@ hipError_t bwd_launch(mbs::bwd::BwdParams &p, bool have_ck, float *dA, float *dB
     }
     if (e != hipSuccess) return e;
     if (nseg > 1) {
-        const dim3 grid_agg((unsigned)((waves * (nseg - 1) + W::kWaves - 1) / W::kWaves));
+        const dim3 grid_agg((unsigned)((waves * p.agg_pieces * (nseg - 1) + W::kWaves - 1) / W::kWaves));
         e = hipLaunchKernel(reinterpret_cast<const void *>(&W::bwd_seg_aggregate<IN, OUT, GATE, SP>), grid_agg,
                             block, args, sizeof(W::AggSmem) * W::kWaves, st);
         if (e != hipSuccess) return e;
@@ -650,13 +661,13 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     }
 
     namespace W = mbs::bwd;
-    int64_t seg_len = L;
-    const int64_t nseg = bwd_segments(B, D, L, &seg_len);
+    int64_t seg_len = L, agg_pieces = 1;
+    const int64_t nseg = bwd_segments(B, D, L, &seg_len, &agg_pieces);
     const int64_t n_cg = bwd_partial_groups(B, D, nseg);       // dB/dC partials per (batch, t)
     const size_t ck_b = ck ? 0 : (size_t)(L / W::kT) * (size_t)rows * W::kN * 4;
     const size_t bcp_b = (size_t)n_cg * (size_t)B * (size_t)L * W::kQ * 4 * 4;
     const size_t row_b = (size_t)nseg * (size_t)rows * (W::kN + 2) * 4;
-    const size_t agg_b = nseg > 1 ? (size_t)nseg * (size_t)rows * W::kN * 2 * 4 : 0;
+    const size_t agg_b = nseg > 1 ? (size_t)(agg_pieces * (nseg - 1)) * (size_t)rows * W::kN * 2 * 4 : 0;
     // The checkpoint pass is a forward recurrence: its pre-pass costs as much per
     // timestep as the pass itself, so it takes the segments only with at most a
     // third as many waves as the chip holds.
@@ -677,6 +688,7 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     p.part_bc = reinterpret_cast<float *>(ws + ck_b);
     p.part_row = reinterpret_cast<float *>(ws + ck_b + bcp_b);
     p.seg_len = seg_len;
+    p.agg_pieces = agg_pieces;
     p.ck_seg_len = ck_nseg > 1 ? seg_len : (L + 31) / 32 * 32;
     p.agg = nseg > 1 ? reinterpret_cast<float *>(ws + ck_b + bcp_b + row_b) : nullptr;
     p.fagg = fagg_b ? reinterpret_cast<float *>(ws + ck_b + bcp_b + row_b + agg_b) : nullptr;

@@ -28,8 +28,8 @@
 //               are deterministic).
 // With few (batch, channel) rows, time is cut into segments so that more waves
 // share the chip: bwd_seg_aggregate runs the adjoint recurrence of every segment
-// but the first from a zero carry, and the wave of segment s starts from
-// dh_last folded with the aggregates of the segments after it.
+// but the first from a zero carry (in pieces), and the wave of segment s starts
+// from dh_last folded with the aggregates of the pieces after it.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -64,14 +64,18 @@ struct BwdParams {
     float *part_row;                   // (nseg, batch * dim, 16 + 2): dA (16), dDskip, dbias per row
                                        // and time segment
     // Time segments (few rows): segment s covers [s seg_len, (s + 1) seg_len) of L.
-    // agg[((s * rows + row) * 16 + n) * 2 + {0, 1}] = (P, H) of segment s >= 1: the
-    // carry abar_{t_b} lambda_{t_b} it hands to segment s - 1 is P c + H, for the
-    // carry c = abar_{t_e} lambda_{t_e} that enters its last timestep.
+    // Segments 1 .. nseg-1 are cut into agg_pieces pieces each, of seg_len /
+    // agg_pieces timesteps (piece i of segment s is number (s - 1) agg_pieces + i;
+    // pieces past L are empty).  agg[((i * rows + row) * 16 + n) * 2 + {0, 1}] =
+    // (P, H) of piece i: the carry abar_{t_b} lambda_{t_b} it hands to the timestep
+    // before it is P c + H, for the carry c = abar_{t_e} lambda_{t_e} that enters its
+    // last timestep.
     // scan_ckpt's own segments, of ck_seg_len (>= L: none):
     // fagg[((s * rows + row) * 16 + n) * 2 + {0, 1}] = the forward aggregate (P, H)
     // of its segment s < nseg - 1 (the forward pre-pass's layout); it starts
     // segment s from h0 folded with those of segments 0 .. s-1.
     int64_t seg_len;
+    int64_t agg_pieces;
     float *agg;
     int64_t ck_seg_len;
     const float *fagg;
@@ -286,14 +290,17 @@ __global__ __launch_bounds__(kThreads) void scan_ckpt(BwdParams p) {
     if (t0 < t_end) chunk(s0, t0);
 }
 
-// ---- the adjoint aggregate of a time segment ---------------------------------------
+// ---- the adjoint aggregate of a piece of a time segment -----------------------------
 // The adjoint recurrence is linear in its carry: within [t_b, t_e),
 // lambda_t = ds_t C_t + carry and the next carry is abar_t lambda_t, so the carry
 // handed on, abar_{t_b} lambda_{t_b}, is P c + H for the carry c entering t_e - 1,
 // with P = prod_t abar_t = 2^(A log2 e sum_t dlt_t) and H the carry from c = 0.
 // (The associative operator of Section 2 applied to the adjoint, backwards.)
 // Lanes own channel j, states 2q, 2q+1 as in scan_bwd; per 16-step chunk the
-// wave stages (dlt, ds) and C, then runs the recurrence backwards.
+// wave stages (dlt, ds) and C, then runs the recurrence backwards.  One wave per
+// piece and 8 channels: with few rows a whole segment per wave would leave a lone
+// wave on a SIMD, which waits on its chain (two dependent operations per step),
+// so the host cuts each segment into up to 4 pieces.
 struct AggSmem {
     float2 dd[kT][kCh + 1];           // (dlt, ds) of timestep t, channel j
     float2 cc[kT][kQ + 1];            // (C[2q], C[2q+1]) at timestep t
@@ -306,15 +313,23 @@ __global__ __launch_bounds__(kThreads) void bwd_seg_aggregate(BwdParams p) {
     const int lane = threadIdx.x & 63, j = lane >> 3, q = lane & 7, n0 = 2 * q;
     const int64_t n_cg = (p.dim + kCh - 1) / kCh, L = p.seqlen;
     const int64_t nseg = (L + p.seg_len - 1) / p.seg_len;
+    const int64_t npieces = p.agg_pieces * (nseg - 1), piece_len = p.seg_len / p.agg_pieces;
     const int64_t wid = wave_id();
-    if (wid >= n_cg * p.batch * (nseg - 1)) return;    // segments 1 .. nseg-1
-    const int64_t cg = wid % n_cg, b = (wid / n_cg) % p.batch, seg = 1 + wid / (n_cg * p.batch);
-    const int64_t t_begin = seg * p.seg_len;
-    const int64_t t_end = t_begin + p.seg_len < L ? t_begin + p.seg_len : L;
+    if (wid >= n_cg * p.batch * npieces) return;       // the pieces of segments 1 .. nseg-1
+    const int64_t cg = wid % n_cg, b = (wid / n_cg) % p.batch, piece = wid / (n_cg * p.batch);
+    const int64_t t_begin = p.seg_len + piece * piece_len;
+    const int64_t t_end = t_begin + piece_len < L ? t_begin + piece_len : L;
     const int64_t d = cg * kCh + j;
     const bool live = d < p.dim;
     const int64_t dcl = live ? d : p.dim - 1;
     const int64_t row = b * p.dim + dcl, rows = p.batch * p.dim;
+    if (t_begin >= L) {                                 // an empty piece of the last segment
+        if (live) {
+            float *o = p.agg + ((piece * rows + row) * kN + n0) * 2;
+            *reinterpret_cast<f32x4 *>(o) = f32x4{1.0f, 0.0f, 1.0f, 0.0f};
+        }
+        return;
+    }
     const float bias = p.dt_bias ? p.dt_bias[dcl] : 0.0f;
     float a2[2], carry[2] = {0.0f, 0.0f}, dsum = 0.0f;
 #pragma unroll
@@ -328,7 +343,7 @@ __global__ __launch_bounds__(kThreads) void bwd_seg_aggregate(BwdParams p) {
 
     // per element: lane (j, q) takes timesteps 2q, 2q+1; C staging: timesteps 2j, 2j+1
     struct Slot { Raw2<IN> dl, z, c0, c1; Raw2<OUT> dy; };
-    auto issue = [&](Slot &sl, int64_t t0) {                // clamped at the segment start
+    auto issue = [&](Slot &sl, int64_t t0) {                // clamped at the piece start
         const uint32_t tc = (uint32_t)(t0 >= t_begin ? t0 : t_begin);
         const uint32_t oa = lrow + tc + 2 * q, ob = brow + tc + 2 * j;
         sl.dl.load(db, oa);
@@ -372,13 +387,13 @@ __global__ __launch_bounds__(kThreads) void bwd_seg_aggregate(BwdParams p) {
     }
     if (t0 >= t_begin) chunk(s0, t0);
 
-    dsum += __shfl_xor(dsum, 1);                         // the segment's sum of dlt for channel j
+    dsum += __shfl_xor(dsum, 1);                         // the piece's sum of dlt for channel j
     dsum += __shfl_xor(dsum, 2);
     dsum += __shfl_xor(dsum, 4);
     if (live) {
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
-            float *o = p.agg + ((seg * rows + row) * kN + n0 + s) * 2;
+            float *o = p.agg + ((piece * rows + row) * kN + n0 + s) * 2;
             o[0] = hw_exp2(a2[s] * dsum);
             o[1] = carry[s];
         }
@@ -420,9 +435,9 @@ __global__ __launch_bounds__(kThreads, 2) void scan_bwd(BwdParams p) {     // 2 
         Av[s] = p.A[dcl * kN + n0 + s];
         a2[s] = Av[s] * kLog2e;
         carry[s] = (p.dh_last && live) ? p.dh_last[row * kN + n0 + s] : 0.0f;   // abar_{t+1} lambda_{t+1}
-        // carry-in: fold the aggregates of the later segments, the last one first
-        for (int64_t s2 = nseg - 1; s2 > seg; --s2) {
-            const float *a = p.agg + ((s2 * rows + row) * kN + n0 + s) * 2;
+        // carry-in: fold the aggregates of the later segments' pieces, the last one first
+        for (int64_t i = p.agg_pieces * (nseg - 1) - 1; i >= p.agg_pieces * seg; --i) {
+            const float *a = p.agg + ((i * rows + row) * kN + n0 + s) * 2;
             carry[s] = live ? __builtin_fmaf(a[0], carry[s], a[1]) : 0.0f;
         }
     }
