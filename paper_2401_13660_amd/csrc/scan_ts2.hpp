@@ -27,7 +27,10 @@
 // plain kernel, so y and h_last are its bits exactly.  The cost over the plain
 // kernel is the chain of slice 0 run twice (one FMA per state and step).
 // Requires seqlen % 16 == 0 and 16-byte aligned activation rows, like the plain
-// kernel; one time segment (the host uses the plain kernel otherwise).
+// kernel; one time segment (the host uses the plain kernel otherwise).  With
+// p.ck it also stores the backward's checkpoints, the state before every 16th
+// timestep, which are the slices' entering states (the same bits as the plain
+// kernel's checkpoints).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -79,7 +82,8 @@ __device__ __forceinline__ float pair_swap(float v) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xf, 0xf, false));
 }
 
-template <int IN, int OUT, bool GATE, bool SOFTPLUS>
+// CK = true: also store the backward's checkpoints in p.ck.
+template <int IN, int OUT, bool GATE, bool SOFTPLUS, bool CK = false>
 __global__ __launch_bounds__(kThreads) void scan_fwd_ts2(ScanParams p) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -104,7 +108,7 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_ts2(ScanParams p) {
     const int64_t d = cg * kCh + j;
     const bool live = d < p.dim;
     const int64_t dcl = live ? d : p.dim - 1;           // dead lanes read a valid row, never store
-    const int64_t row = b * p.dim + dcl;
+    const int64_t row = b * p.dim + dcl, rows = p.batch * p.dim;
     const int64_t L = p.seqlen;
     const int n0 = 2 * q;
 
@@ -252,6 +256,11 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_ts2(ScanParams p) {
             g[0] = k ? e0 : h[0];
             g[1] = k ? e1 : h[1];
         }
+        // checkpoints for the backward: the states before timesteps t0 and t0 + 16
+        // are the two slices' entering states
+        if (CK && live && t0 + kS * k < seq_n)
+            *reinterpret_cast<float2 *>(p.ck + (((int64_t)(t0 / kS) + k) * rows + row) * kN + n0) =
+                float2{g[0], g[1]};
 
         // ---- T: the chain again from the true entering state, with the partials
         {
@@ -323,11 +332,12 @@ __global__ __launch_bounds__(kThreads) void scan_fwd_ts2(ScanParams p) {
 namespace mbs {
 namespace ts2 {
 
-// Whether the time-split kernel takes p: one time segment, no recorded states
-// or checkpoints, at least one full chunk, and no more plain-kernel waves than
-// SIMDs (where the plain kernel would leave every SIMD with one wave at most).
+// Whether the time-split kernel takes p: one time segment, no recorded states,
+// at least one full chunk, and no more plain-kernel waves than SIMDs (where the
+// plain kernel would leave every SIMD with one wave at most).  Checkpoints (p.ck)
+// are the slices' entering states, stored after the hand-over.
 inline bool takes(const ScanParams &p) {
-    if (p.npos > 0 || p.ck || p.seqlen < kT) return false;
+    if (p.npos > 0 || p.seqlen < kT) return false;
     int64_t seg_len, pieces;
     if (tiled::fwd_segments(p, &seg_len, &pieces) != 1) return false;
     const int64_t plain_waves = (p.dim + tiled::kCh - 1) / tiled::kCh * p.batch;
@@ -339,8 +349,11 @@ hipError_t fwd_ts2(ScanParams &p, void *stream) {
     const int64_t waves = (p.dim + kCh - 1) / kCh * p.batch;
     const int64_t blocks = (waves + kWavesPerGroup - 1) / kWavesPerGroup;
     void *args[] = {&p};
-    const void *fn = p.delta_softplus ? reinterpret_cast<const void *>(&scan_fwd_ts2<IN, OUT, GATE, true>)
-                                      : reinterpret_cast<const void *>(&scan_fwd_ts2<IN, OUT, GATE, false>);
+    const void *fn =
+        p.ck ? (p.delta_softplus ? reinterpret_cast<const void *>(&scan_fwd_ts2<IN, OUT, GATE, true, true>)
+                                 : reinterpret_cast<const void *>(&scan_fwd_ts2<IN, OUT, GATE, false, true>))
+             : (p.delta_softplus ? reinterpret_cast<const void *>(&scan_fwd_ts2<IN, OUT, GATE, true>)
+                                 : reinterpret_cast<const void *>(&scan_fwd_ts2<IN, OUT, GATE, false>));
     return hipLaunchKernel(fn, dim3((unsigned)blocks), dim3(kThreads), args, sizeof(WaveSmem) * kWavesPerGroup,
                            static_cast<hipStream_t>(stream));
 }

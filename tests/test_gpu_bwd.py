@@ -165,9 +165,11 @@ def _fwd_ckpt(t):
     return ck
 
 
-# (batch, dim, L): whole 32-step chunks with dead lanes; a trailing half chunk;
-# one row group cut into time segments (the forward's pre-pass path).
-@pytest.mark.parametrize("shape", [(2, 196, 512), (3, 100, 208), (1, 64, 1024)])
+# (batch, dim, L): whole 32-step chunks with dead lanes; a trailing half chunk
+# (the time-split kernel: 39 plain waves); one row group cut into time segments
+# (the forward's pre-pass path); the 353M layer's width (the time-split kernel,
+# 1,024 plain waves), whose slices' entering states are the checkpoints.
+@pytest.mark.parametrize("shape", [(2, 196, 512), (3, 100, 208), (1, 64, 1024), (4, 2048, 1024)])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_fwd_checkpoints_match_oracle_states(shape, dtype):
     """ck[k] is the state before timestep 16k: the oracle's state at position 16k - 1."""
@@ -185,7 +187,7 @@ def test_fwd_checkpoints_match_oracle_states(shape, dtype):
 
 
 @pytest.mark.parametrize("shape,gated", [((2, 196, 512), True), ((1, 64, 1024), False), ((9, 1001, 64), True),
-                                         ((12, 1024, 32), True)])
+                                         ((12, 1024, 32), True), ((4, 2048, 256), True)])
 def test_bwd_from_forward_checkpoints(shape, gated):
     """The backward from the forward's checkpoints: oracle parity, and the same
     gradients as the backward that recomputes its checkpoints."""
