@@ -323,10 +323,14 @@ __global__ __launch_bounds__(kThreads) void bwd_seg_aggregate(BwdParams p) {
     const bool live = d < p.dim;
     const int64_t dcl = live ? d : p.dim - 1;
     const int64_t row = b * p.dim + dcl, rows = p.batch * p.dim;
-    if (t_begin >= L) {                                 // an empty piece of the last segment
+    if (t_begin >= L) {                                 // an empty piece of the last segment: (1, 0)
         if (live) {
-            float *o = p.agg + ((piece * rows + row) * kN + n0) * 2;
-            *reinterpret_cast<f32x4 *>(o) = f32x4{1.0f, 0.0f, 1.0f, 0.0f};
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {                 // (the planes are 8-byte aligned only)
+                float *o = p.agg + ((piece * rows + row) * kN + n0 + s) * 2;
+                o[0] = 1.0f;
+                o[1] = 0.0f;
+            }
         }
         return;
     }
