@@ -664,17 +664,20 @@ int mb_scan_bwd(const mb_scan_desc *desc, const void *u, const void *delta, cons
     int64_t seg_len = L, agg_pieces = 1;
     const int64_t nseg = bwd_segments(B, D, L, &seg_len, &agg_pieces);
     const int64_t n_cg = bwd_partial_groups(B, D, nseg);       // dB/dC partials per (batch, t)
-    const size_t ck_b = ck ? 0 : (size_t)(L / W::kT) * (size_t)rows * W::kN * 4;
-    const size_t bcp_b = (size_t)n_cg * (size_t)B * (size_t)L * W::kQ * 4 * 4;
-    const size_t row_b = (size_t)nseg * (size_t)rows * (W::kN + 2) * 4;
-    const size_t agg_b = nseg > 1 ? (size_t)(agg_pieces * (nseg - 1)) * (size_t)rows * W::kN * 2 * 4 : 0;
+    // each area of the workspace starts on a 256-byte boundary (the kernels move
+    // 16-byte vectors in the partials and the forward aggregates)
+    auto pad = [](size_t n) { return (n + 255) / 256 * 256; };
+    const size_t ck_b = ck ? 0 : pad((size_t)(L / W::kT) * (size_t)rows * W::kN * 4);
+    const size_t bcp_b = pad((size_t)n_cg * (size_t)B * (size_t)L * W::kQ * 4 * 4);
+    const size_t row_b = pad((size_t)nseg * (size_t)rows * (W::kN + 2) * 4);
+    const size_t agg_b = nseg > 1 ? pad((size_t)(agg_pieces * (nseg - 1)) * (size_t)rows * W::kN * 2 * 4) : 0;
     // The checkpoint pass is a forward recurrence: its pre-pass costs as much per
     // timestep as the pass itself, so it takes the segments only with at most a
     // third as many waves as the chip holds.
     const int64_t ck_nseg = (!ck && 3 * ((D + W::kCh - 1) / W::kCh * B) <= mbs::tiled::resident_waves()) ? nseg : 1;
     // the forward pre-pass writes ck_nseg planes: the aggregates of segments
     // 0 .. ck_nseg-2 and a copy of h0 (which scan_ckpt does not need)
-    const size_t fagg_b = ck_nseg > 1 ? (size_t)ck_nseg * (size_t)rows * W::kN * 2 * 4 : 0;
+    const size_t fagg_b = ck_nseg > 1 ? pad((size_t)ck_nseg * (size_t)rows * W::kN * 2 * 4) : 0;
     char *ws = nullptr;
     e = hipMallocAsync(reinterpret_cast<void **>(&ws), ck_b + bcp_b + row_b + agg_b + fagg_b, st);
     if (e != hipSuccess) return MB_ERR_HIP;
